@@ -1,0 +1,187 @@
+"""Seeded synthetic inputs for the cached DiT block step.
+
+Both the CPU oracle and the GPU path consume exactly these arrays.  This module
+holds no arithmetic of the method itself: it draws audio, latents, weights and
+modulation vectors, and rounds inputs to the storage precision (bf16, round to
+nearest even) so that both sides see identical values.
+
+Every draw uses ``np.random.default_rng([seed, stream])`` with a fixed stream
+number per tensor family, so any tensor can be regenerated on its own.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .configs import Workload
+
+STREAM_WEIGHTS, STREAM_BIAS, STREAM_MOD, STREAM_XREF, STREAM_DRIFT, STREAM_AUDIO = 1, 2, 3, 4, 5, 6
+
+
+def _rng(seed: int, stream: int, sub: int = 0) -> np.random.Generator:
+    return np.random.default_rng([seed, stream, sub])
+
+
+# ---------------------------------------------------------------- bf16 storage
+
+def to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns (uint16), round to nearest even.  Used only
+    to put inputs into their storage precision."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32)
+    lsb = (u >> 16) & np.uint32(1)
+    # wraps only for negative NaN patterns, which are overwritten below
+    r = ((u + np.uint32(0x7FFF) + lsb) >> 16).astype(np.uint16)
+    nan = np.isnan(a)
+    if nan.any():
+        r[nan] = 0x7FC0
+    return r
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def storage_round(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Round an fp32 array to what the device stores (fp32 or bf16), returned
+    as fp32 values."""
+    a = np.asarray(a, dtype=np.float32)
+    if dtype == "f32":
+        return a
+    if dtype == "bf16":
+        return bf16_bits_to_f32(to_bf16_bits(a))
+    raise ValueError(dtype)
+
+
+# ---------------------------------------------------------------------- audio
+
+def _raised_cos_env(n: int, edge: int) -> np.ndarray:
+    env = np.ones(n)
+    e = min(edge, n // 2)
+    if e > 0:
+        ramp = 0.5 - 0.5 * np.cos(np.pi * np.arange(e) / e)
+        env[:e] = ramp
+        env[n - e:] = ramp[::-1]
+    return env
+
+
+def _burst(rng, n, sr, speech: bool) -> np.ndarray:
+    t = np.arange(n) / sr
+    f0 = rng.uniform(90.0, 250.0)
+    if speech:
+        inst = f0 * (1.0 + 0.1 * np.sin(2 * np.pi * 0.5 * t))
+        phase0 = 2 * np.pi * np.cumsum(inst) / sr
+    else:
+        phase0 = 2 * np.pi * f0 * t
+    sig = np.zeros(n)
+    for h in range(1, 7):
+        sig += np.cos(h * phase0 + rng.uniform(0, 2 * np.pi)) / h
+    am_rate = rng.uniform(4.0, 5.0) if speech else rng.uniform(3.0, 6.0)
+    sig *= 1.0 - 0.5 * (0.5 - 0.5 * np.cos(2 * np.pi * am_rate * t))
+    if speech:
+        # fricative-like noise bursts of 30-80 ms at level 0.1
+        n_fric = rng.integers(0, 3)
+        for _ in range(int(n_fric)):
+            ln = int(rng.uniform(0.03, 0.08) * sr)
+            if ln >= n:
+                continue
+            s0 = int(rng.integers(0, n - ln))
+            noise = rng.standard_normal(ln)
+            noise = np.convolve(noise, np.ones(4) / 4, mode="same")
+            sig[s0:s0 + ln] += 0.1 * noise * _raised_cos_env(ln, ln // 4)
+    sig *= _raised_cos_env(n, int(0.02 * sr))
+    peak = np.max(np.abs(sig))
+    if peak > 0:
+        sig *= rng.uniform(0.2, 1.0) / peak
+    return sig
+
+
+def make_audio(profile: str, n_samples: int, sr: int, seed: int) -> np.ndarray:
+    """Synthetic mono audio in [-1, 1], fp32.
+
+    bursts        amplitude-modulated harmonic bursts (6 harmonics, 1/h) of
+                  0.15-0.5 s separated by exact-zero silences of 0.05-0.35 s
+    speech        bursts with an f0 glide, syllable-rate AM, fricative noise
+                  and pauses of 0.1-0.4 s
+    noise         white noise N(0, 0.1^2): flat energy
+    half_silence  exact zeros for the first half, speech after
+    """
+    rng = _rng(seed, STREAM_AUDIO)
+    if profile == "noise":
+        return np.clip(0.1 * rng.standard_normal(n_samples), -1, 1).astype(np.float32)
+    if profile == "half_silence":
+        a = make_audio("speech", n_samples, sr, seed)
+        a[: n_samples // 2] = 0.0
+        return a
+    speech = profile == "speech"
+    if profile not in ("bursts", "speech"):
+        raise ValueError(profile)
+    out = np.zeros(n_samples)
+    pos = 0
+    while pos < n_samples:
+        burst = int(rng.uniform(0.15, 0.5) * sr)
+        b = _burst(rng, min(burst, n_samples - pos), sr, speech)
+        out[pos:pos + len(b)] = b
+        pos += len(b)
+        gap = rng.uniform(0.1, 0.4) if speech else rng.uniform(0.05, 0.35)
+        pos += int(gap * sr)
+    return np.clip(out, -1, 1).astype(np.float32)
+
+
+# -------------------------------------------------------------------- latents
+
+def make_latents(w: Workload, seed: int | None = None):
+    """(xref, x): the cached block input and the current step's block input,
+    [L, D] fp32 holding storage-rounded values.
+
+    xref ~ N(0, 1); x = xref + sigma_f * N(0, 1) with one sigma_f ~ U(0.01, 0.3)
+    per latent frame, so frames drift by different amounts.
+    """
+    seed = w.seed if seed is None else seed
+    rx = _rng(seed, STREAM_XREF)
+    xref = rx.standard_normal((w.L, w.D), dtype=np.float32)
+    rd = _rng(seed, STREAM_DRIFT)
+    sigma = rd.uniform(0.01, 0.3, size=w.T).astype(np.float32)
+    noise = rd.standard_normal((w.L, w.D), dtype=np.float32)
+    x = xref + np.repeat(sigma, w.N)[:, None] * noise
+    return storage_round(xref, w.dtype), storage_round(x, w.dtype)
+
+
+def make_block_weights(w: Workload, seed: int | None = None, gate_mean=None,
+                       gate_std=None) -> dict:
+    """DiT block parameters in nn.Linear layout ([out, in]).
+
+    Linear weights and biases ~ N(0, 0.02); modulation rows (shift1, scale1,
+    gate1, shift2, scale2, gate2): shifts and scales ~ N(0, 0.1), gates
+    ~ N(gate_mean, gate_std).  Weights, biases and modulation are rounded to
+    the storage dtype (modulation stays fp32 on the device but is rounded the
+    same way so both sides see one value).
+    """
+    seed = w.seed if seed is None else seed
+    gm = w.gate_mean if gate_mean is None else gate_mean
+    gs = w.gate_std if gate_std is None else gate_std
+    D, F = w.D, w.F
+    shapes = {"wq": (D, D), "wk": (D, D), "wv": (D, D), "wo": (D, D),
+              "w1": (F, D), "w2": (D, F)}
+    out = {}
+    for i, (k, shp) in enumerate(shapes.items()):
+        r = _rng(seed, STREAM_WEIGHTS, i)
+        out[k] = storage_round(0.02 * r.standard_normal(shp, dtype=np.float32), w.dtype)
+    bshapes = {"bq": D, "bk": D, "bv": D, "bo": D, "b1": F, "b2": D}
+    for i, (k, n) in enumerate(bshapes.items()):
+        r = _rng(seed, STREAM_BIAS, i)
+        out[k] = storage_round(0.02 * r.standard_normal(n, dtype=np.float32), w.dtype)
+    r = _rng(seed, STREAM_MOD)
+    mod = np.empty((6, D), dtype=np.float32)
+    for row in range(6):
+        if row in (2, 5):
+            mod[row] = gm + gs * r.standard_normal(D)
+        else:
+            mod[row] = 0.1 * r.standard_normal(D)
+    out["mod"] = storage_round(mod, w.dtype)
+    return out
+
+
+def random_frame_weight(T: int, seed: int) -> np.ndarray:
+    """Arbitrary per-frame weights in [0, 1] (for selection tests that do not
+    go through the audio path)."""
+    return _rng(seed, 99).uniform(0.0, 1.0, size=T).astype(np.float32)
