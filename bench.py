@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Throughput of one cached DiT block step on one MI355X.
+
+A step is the whole hot path on one batch of synthetic input, resident in HBM:
+audio energy (echo_energy), saliency + top-K selection (echo_select), the DiT
+block on the selected tokens (echo_block_partial) and the int8 cache update
+with reuse of every other token (echo_cache_update).  The default workload is
+the Wan2.2-S2V-14B-shaped block at 480p: 21 latent frames x 30 x 52 = 32760
+tokens, hidden 5120, 40 heads of 128, FFN 13824, recompute ratio 0.4 (13104
+tokens), 5.06 s of 16 kHz audio.
+
+Prints one JSON line: whole-step tokens/s (L / step time), the roofline of the
+dominant kernel measured with HIP events on the launch stream during the timed
+steps, a per-kernel table, and the CPU oracle's throughput on a bounded sample
+(rank 0, N = 1).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "latent tokens/s per cached DiT block step + %MFMA / %HBM peak"
+KERNEL_SOURCES = {"attn_fwd": "attn_bf16.hip", "gemm_": "gemm_bf16.hip", "saliency": "select.hip",
+                  "select": "select.hip", "cache_update": "cache.hip", "modln": "block_ln.hip",
+                  "energy": "energy.hip"}
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_sha(kernel: str) -> str | None:
+    for prefix, fname in KERNEL_SOURCES.items():
+        if kernel.startswith(prefix):
+            path = os.path.join(ROOT, "paper_2608_02474_amd", "csrc", fname)
+            return hashlib.sha256(open(path, "rb").read()).hexdigest()
+    return None
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current source of that kernel; None otherwise."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(kernel)
+    if not rec or rec.get("source_sha256") != source_sha(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def _timed(fn, *a) -> float:
+    """Seconds of fn(*a) on its second run: the first run pays one-time costs
+    (page faults of fresh allocations) that are not part of the work."""
+    fn(*a)
+    t0 = time.perf_counter()
+    fn(*a)
+    return time.perf_counter() - t0
+
+
+def _fit_time(fn, r1: int, r2: int, full: int) -> float:
+    """Time fn(r) at two sample sizes and extrapolate t = fixed + per_row * r
+    to r = full, so per-call overheads are not multiplied by the row count."""
+    t1 = _timed(fn, r1)
+    t2 = _timed(fn, r2)
+    per_row = max(t2 - t1, 0.0) / (r2 - r1)
+    fixed = max(t1 - per_row * r1, 0.0)
+    return fixed + per_row * full
+
+
+def cpu_baseline(w, p, x, xref, audio):
+    """The CPU oracle, as it stands, timed on bounded samples of the workload;
+    each part is extrapolated to the full step from two sample sizes."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import block as OB
+    from oracle import cache as OC
+    from oracle import energy as OE
+    from oracle import select as OS
+
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    L, D, K = w.L, w.D, w.K
+    p64 = OB._f64(p)                      # weights held in fp64 once (setup, not timed)
+    t = {}
+    fw = OE.energy(audio, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)[2]
+    t["energy"] = _timed(OE.energy, audio, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
+    r_sal, r_kv, r_cache = min(L, 4096), min(L, 2048), min(L, 4096)
+    t["saliency"] = _timed(OS.saliency, x[:r_sal], xref[:r_sal], fw, w.N) * L / r_sal
+    s_full = np.resize(OS.saliency(x[:r_sal], xref[:r_sal], fw, w.N)[0], L)
+    t["topk"] = _timed(OS.select_topk, s_full, K)
+    x64 = np.asarray(x[:r_kv], np.float64)
+    t["ln_kv"] = _timed(OB.kv_projection, p64, x64) * L / r_kv
+    kv = OB.kv_projection(p64, x64)
+    # keys/values of all L rows, tiled from the projected sample (timing only)
+    reps = -(-L // r_kv)
+    kv_full = tuple(np.concatenate([m] * reps)[:L] for m in kv)
+    del kv, x64
+
+    def sel_rows(r):
+        OB.block_partial(p64, x[:r], np.arange(r), w.H, kv=kv_full)
+    r_sel = (min(K, 64), min(K, 256))
+    t["selected_rows"] = _fit_time(sel_rows, r_sel[0], r_sel[1], K)
+    del kv_full
+    k_c = max(1, r_cache * K // L)
+    idx = np.linspace(0, r_cache - 1, k_c).astype(np.int64)
+    t["cache_update"] = _timed(OC.cache_update, x[:r_cache], idx, x[idx] + np.float32(0.01),
+                               xref[:r_cache], np.zeros((r_cache, D), np.int8),
+                               np.zeros(r_cache, np.float32), w.dtype) * L / r_cache
+    total = sum(t.values())
+    return {"value": L / total, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"fp64 numpy oracle: full audio energy; saliency of {r_sal} rows; a full "
+                       f"{L}-key top-{K}; LN + K/V projection of {r_kv} rows; {r_sel[0]} and "
+                       f"{r_sel[1]} selected rows (Q, attention over all {L} keys, O, FFN); cache "
+                       f"update of {r_cache} rows. Row-proportional parts are scaled by rows; the "
+                       f"selected-row part is extrapolated as fixed + per-row cost"),
+            "step_seconds": total, "parts_seconds": {k_: round(v_, 3) for k_, v_ in t.items()}}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="wan14b_480p_32760tok")
+    ap.add_argument("--skip-cpu-baseline", action="store_true",
+                    help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
+                         "unchanged")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the cached block step runs on a single MI355X "
+              "(multi-GPU sharding is designed, not built). Run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_02474_amd import api, roofline
+
+    if args.workload not in synth.ALL:
+        print(f"unknown workload {args.workload}; choose from {sorted(synth.ALL)}", file=sys.stderr)
+        return 2
+    w = synth.ALL[args.workload]
+    dev = torch.device("cuda:0")
+    dt = {"bf16": torch.bfloat16, "f32": torch.float32}[w.dtype]
+    b = 2 if w.dtype == "bf16" else 4
+
+    log(f"workload {w.name}: L={w.L} K={w.K} D={w.D} H={w.H} F={w.F}; generating inputs")
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    audio = synth.make_audio(w.audio, w.n_samples, w.sample_rate, w.seed)
+    P = {k: torch.from_numpy(v).to(torch.float32 if k == "mod" else dt).to(dev) for k, v in p.items()}
+    X = torch.from_numpy(x).to(dt).to(dev)
+    XR = torch.from_numpy(xref).to(dt).to(dev)
+    A = torch.from_numpy(audio).to(dev)
+
+    blk = api.CachedBlock(P, w.H, w.L, w.D, dev, dt)
+    blk.init(XR)                              # fill the cache: every token recomputed once
+    torch.cuda.synchronize()
+
+    def step():
+        _, _, fw = api.energy(A, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
+        return blk.step(X, fw, w.N, k=w.K)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    api.profile_enable(True)
+    api.profile_read()                        # drop anything recorded so far
+    log(f"timing {args.steps} steps")
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    ktimes = api.profile_read()
+    api.profile_enable(False)
+
+    work = roofline.kernel_work(w.L, w.K, w.D, w.F, b, w.n_samples)
+    kernels = {}
+    for name, (launches, total_ms) in sorted(ktimes.items(), key=lambda kv: -kv[1][1]):
+        avg = total_ms / launches
+        wk = roofline.work_of(name, work)
+        entry = {"avg_ms": round(avg, 4), "launches": launches,
+                 "share": round(total_ms / (ms * args.steps), 4)}
+        if wk is not None and wk[0] > 0:
+            amount, kind = wk
+            if kind == "flop":
+                ach = amount / (avg * 1e-3) / 1e12
+                entry.update(achieved=round(ach, 2), unit="TFLOP/s",
+                             frac=round(ach / roofline.PEAK_BF16_TFLOPS, 4), per_launch=amount)
+            else:
+                ach = amount / (avg * 1e-3) / 1e9
+                entry.update(achieved=round(ach, 1), unit="GB/s",
+                             frac=round(ach / roofline.PEAK_HBM_GBS, 4), per_launch=amount)
+        kernels[name] = entry
+
+    dom = max(ktimes, key=lambda n: ktimes[n][1])
+    d = kernels[dom]
+    roof = {"kernel": dom, "bound": "mfma" if d.get("unit") == "TFLOP/s" else "hbm",
+            "achieved": d.get("achieved"), "peak": (roofline.PEAK_BF16_TFLOPS if d.get("unit") ==
+                                                     "TFLOP/s" else roofline.PEAK_HBM_GBS),
+            "unit": d.get("unit"), "frac": d.get("frac"), "per_launch": d.get("per_launch"),
+            "avg_ms": d["avg_ms"], "traffic": measured_traffic(dom)}
+
+    block_names = [n for n in ktimes if n.startswith(("modln", "gemm_", "attn_fwd"))]
+    block_ms = sum(ktimes[n][1] for n in block_names) / args.steps
+    block_tf = roofline.block_flops(w.L, w.K, w.D, w.F) / (block_ms * 1e-3) / 1e12
+    sal = kernels.get("saliency_rows_bf16") or kernels.get("saliency_rows_f32") or {}
+    cache = kernels.get("cache_update_bf16") or kernels.get("cache_update_f32") or {}
+
+    out = {
+        "metric": METRIC, "value": round(w.L / (ms * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded; Wan2.2-S2V-shaped latents, random-init block weights, "
+                "speech-like audio)",
+        "config": {"workload": w.name, "tokens": w.L, "recomputed_tokens": w.K, "ratio": w.ratio,
+                   "latent_frames": w.T, "grid": list(w.grid), "hidden": w.D, "heads": w.H,
+                   "ffn": w.F, "audio_samples": w.n_samples},
+        "recomputed_tokens_per_s": round(w.K / (ms * 1e-3), 1),
+        "roofline": roof,
+        "block_partial": {"ms": round(block_ms, 4), "tflops": round(block_tf, 2),
+                          "frac_bf16_peak": round(block_tf / roofline.PEAK_BF16_TFLOPS, 4)},
+        "select_hbm_frac": sal.get("frac"), "cache_hbm_frac": cache.get("frac"),
+        "kernels": kernels,
+    }
+    if not torch.isfinite(blk.y.float()).all():
+        log("non-finite block output")
+        return 1
+
+    if args.skip_cpu_baseline:
+        out["cpu_baseline"] = None
+    else:
+        log("CPU oracle baseline on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(w, p, x, xref, audio)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

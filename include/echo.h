@@ -1,0 +1,218 @@
+/*
+ * echo.h -- C ABI of libecho, the MI355X (gfx950) implementation of the cached
+ * DiT block step of EchoCache (energy-guided cross-modal caching for
+ * audio-driven video generation).
+ *
+ * One step of the method, for one DiT block, is four calls:
+ *
+ *   echo_energy        audio -> per-latent-frame energy and weight
+ *                      (Sec. 3.3, "Cross-modal Saliency Anchors"; once per clip)
+ *   echo_select        per-token saliency = frame weight x relative change of the
+ *                      block input against its cached input (Sec. 3.1 Eq. 1),
+ *                      then top-K (or threshold) selection of tokens to recompute
+ *                      (Sec. 3.3, saliency mask and k_t = ceil(N r_t))
+ *   echo_block_partial the DiT block on the selected tokens only: queries from the
+ *                      selected tokens, keys/values from all tokens, FFN on the
+ *                      selected tokens (Sec. 3.3, "Fine-grained latent-level caching")
+ *   echo_cache_update  int8 residual cache write for the selected tokens and
+ *                      dequantized reuse for all others, fused into the block output
+ *                      (Sec. 3.3 mask fusion; Sec. 3.4 reference + int8 residual)
+ *
+ * Conventions shared by every call
+ *   - Tensor pointers are DEVICE pointers on the current HIP device, owned by
+ *     the caller, row-major and 16-byte aligned.  The library allocates no
+ *     memory: scratch space is a caller-provided workspace whose size the
+ *     matching *_workspace() query returns.
+ *   - Every call is asynchronous on `stream` (a hipStream_t passed as void*,
+ *     NULL = the null stream) and never synchronises the host.
+ *   - Arguments are validated before any HIP call; a rejected call launches
+ *     nothing and writes nothing.  Errors are returned as echo_status codes;
+ *     nothing throws across the ABI.  After ECHO_EDEVICE,
+ *     echo_last_hip_error() returns the hipError_t of the failure (per thread).
+ *   - Activation/weight storage is ECHO_F32 or ECHO_BF16 (bf16 = the upper 16
+ *     bits of an IEEE fp32).  Accumulation is fp32 (fp64 where stated).
+ *   - Token layout: L = T * N tokens, frame-major (token i is in latent frame
+ *     floor(i / N)); one batch element.
+ */
+#ifndef ECHO_H
+#define ECHO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ECHO_OK = 0,
+  ECHO_EINVAL = 1,        /* null/misaligned pointer, size out of range, bad shape */
+  ECHO_EUNSUPPORTED = 2,  /* well-formed but outside the supported shapes/dtypes   */
+  ECHO_EWORKSPACE = 3,    /* workspace pointer null or smaller than required       */
+  ECHO_EDEVICE = 4        /* a HIP call failed; see echo_last_hip_error()          */
+} echo_status;
+
+typedef enum { ECHO_F32 = 0, ECHO_BF16 = 1 } echo_dtype;
+
+/* Static string for a status code (never NULL). */
+const char* echo_status_str(int status);
+/* hipError_t of the last ECHO_EDEVICE on the calling thread (0 if none). */
+int echo_last_hip_error(void);
+/* Library version string, e.g. "0.1.0". */
+const char* echo_version(void);
+
+/* ------------------------------------------------------------------ energy */
+/*
+ * Audio energy anchor (Sec. 3.3, "Cross-modal Saliency Anchors").  The clip of
+ * n_samples is split into T even segments, segment t = samples
+ * [floor(t n / T), floor((t+1) n / T)); each segment gets an STFT (periodic
+ * Hann window of n_fft, hop `hop`, no centring; a segment shorter than n_fft is
+ * zero-padded to one frame; one-sided bins 0..n_fft/2).  Outputs (fp32):
+ *   band_energy [T][n_bands]  sum of |X|^2 over the frames of segment t and the
+ *                             bins of band b; bands have equal width on the mel
+ *                             scale 2595 log10(1 + f/700) from 0 to sr/2
+ *   frame_energy [T]          e_t = Frobenius norm of segment t's STFT
+ *                             (= sqrt(sum_b band_energy[t][b]))
+ *   frame_weight [T]          e_t / max_u e_u, or 1 for every t if all e are 0
+ * Computed in fp64, rounded to fp32 once.  Requires 1 <= T <= 65535,
+ * n_samples >= T, n_fft even in [16, 2048], 1 <= hop, 1 <= n_bands <= 64,
+ * sample_rate > 0.  audio: device fp32 [n_samples].
+ */
+typedef struct {
+  int32_t T;
+  int32_t sample_rate;
+  int32_t n_fft;
+  int32_t hop;
+  int32_t n_bands;
+} echo_energy_cfg;
+
+size_t echo_energy_workspace(const echo_energy_cfg* cfg, int64_t n_samples);
+int echo_energy(const echo_energy_cfg* cfg, const float* audio, int64_t n_samples,
+                float* band_energy, float* frame_energy, float* frame_weight,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ select */
+/*
+ * Saliency and recompute selection (Sec. 3.1 Eq. 1 per token; Sec. 3.3).
+ *   delta_i = ||x_i - xref_i||_1 / (||xref_i||_1 + xi)   (fp64 sums)
+ *   s_i     = fp32( fp64(frame_weight[floor(i / N)]) * delta_i )
+ * Top-K mode (k >= 0): the k tokens first in the order (s descending, token
+ * index ascending; a NaN s ranks above every number, -0 equals +0).
+ * Threshold mode (k < 0): every token with s > threshold (or NaN s).
+ * Outputs:
+ *   idx [L] int32        the n_sel selected token indices, ascending, in
+ *                        idx[0..n_sel); entries past n_sel are unspecified
+ *   mask [L] uint8       1 for a selected token, 0 otherwise
+ *   n_sel [1] int32      device scalar, the number selected (== k in top-K mode)
+ *   saliency [L] fp32    s (optional, may be NULL)
+ *   step_delta [1] fp64  sum_i num_i / (sum_i den_i + xi), the step-level Eq. 1
+ *                        value against the cache (optional, may be NULL)
+ * x, xref: [L][D] of `dtype`; frame_weight: fp32 [T].  Requires T, N >= 1,
+ * L = T*N < 2^31, D >= 8 and D % 8 == 0, 0 <= k <= L or k < 0, xi >= 0.
+ */
+typedef struct {
+  int32_t T;
+  int32_t N;
+  int32_t D;
+  int32_t dtype;      /* echo_dtype of x and xref */
+  int32_t k;          /* >= 0: top-k; < 0: threshold mode */
+  float threshold;    /* threshold mode only */
+  double xi;          /* Eq. 1 stabiliser, e.g. 1e-6 */
+} echo_select_cfg;
+
+size_t echo_select_workspace(const echo_select_cfg* cfg);
+int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref,
+                const float* frame_weight, int32_t* idx, uint8_t* mask, int32_t* n_sel,
+                float* saliency, double* step_delta,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------ block partial */
+/*
+ * One adaLN DiT block on the selected tokens only (Sec. 3.3, "Fine-grained
+ * latent-level caching": queries for the active tokens, keys and values from
+ * the complete token set, attention on (Q', K, V), FFN on the active tokens):
+ *   a    = LN(x) * (1 + scale1) + shift1                 all L rows
+ *   q    = a[idx] Wq^T + bq ;  k = a Wk^T + bk ;  v = a Wv^T + bv
+ *   o    = per-head softmax(q k^T / sqrt(D/H)) v          over all L keys
+ *   x1   = x[idx] + gate1 * (o Wo^T + bo)
+ *   y_sel= x1 + gate2 * (GELU_tanh(LN2(x1) W1^T + b1) W2^T + b2),
+ *          LN2(z) = LN(z) * (1 + scale2) + shift2
+ * LN: no affine, biased variance, eps = cfg->ln_eps.  Weights are [out][in]
+ * (nn.Linear layout) in `dtype`: wq, wk, wv, wo [D][D]; w1 [F][D]; w2 [D][F];
+ * biases bq, bk, bv, bo, b2 [D], b1 [F] in `dtype`; mod fp32 [6][D] = rows
+ * shift1, scale1, gate1, shift2, scale2, gate2.
+ * x [L][D] in `dtype`; idx [n_sel] int32 in [0, L) (any order, repeats allowed);
+ * y_sel [n_sel][D] fp32, row j = output of token idx[j].  n_sel = 0 is a no-op.
+ * Supported: ECHO_BF16 with D/H == 128, D % 256 == 0, F % 256 == 0 (bf16
+ * MFMA path); ECHO_F32 with D % 4 == 0, (D/H) % 4 == 0, D/H <= 128,
+ * F % 4 == 0 (fp32 path for small shapes).  D <= 16384, F <= 65536.
+ */
+typedef struct {
+  int32_t L;
+  int32_t D;
+  int32_t H;
+  int32_t F;
+  int32_t dtype;
+  float ln_eps;
+} echo_block_cfg;
+
+typedef struct {
+  const void* wq; const void* wk; const void* wv; const void* wo;
+  const void* w1; const void* w2;
+  const void* bq; const void* bk; const void* bv; const void* bo;
+  const void* b1; const void* b2;
+  const float* mod;
+} echo_block_weights;
+
+size_t echo_block_workspace(const echo_block_cfg* cfg, int32_t n_sel_max);
+int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w,
+                       const void* x, const int32_t* idx, int32_t n_sel, float* y_sel,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------- cache update */
+/*
+ * Cache write and mask fusion (Sec. 3.3: out = m * fresh + (1 - m) * cached;
+ * Sec. 3.4: cached output = reference + dequantized int8 residual, converted
+ * back to the compute precision).  One reference per token, xref_i = the block
+ * input at its last recompute.  For each selected row i = idx[j]:
+ *   res = fp32(y_sel[j] - x_i); amax = max|res|;
+ *   scale_i = fp32(amax / 127); code = clamp(rint(fp32(res * fp32(127 / amax))), +-127)
+ *   (amax == 0 -> scale 0, codes 0); xref_i = x_i; y_i = cast(y_sel[j])
+ * For each unselected row (mask == 0): y_i = cast(fp32(xref_i + fp32(scale_i * code)))
+ * cast = round to nearest even into `dtype`.  x, xref, y: [L][D] `dtype`;
+ * codes [L][D] int8; scale [L] fp32; xref, codes and scale are updated in place.
+ * idx must hold n_sel distinct rows and mask must be their indicator.
+ * Requires D % 8 == 0, D <= 16384.
+ */
+typedef struct {
+  int32_t L;
+  int32_t D;
+  int32_t dtype;
+} echo_cache_cfg;
+
+int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* idx,
+                      const uint8_t* mask, int32_t n_sel, const float* y_sel,
+                      void* xref, int8_t* codes, float* scale, void* y, void* stream);
+
+/* ------------------------------------------------------------ kernel timing */
+/*
+ * Optional per-kernel timing with HIP events, for the calling thread.
+ * echo_profile_enable(1) makes every later launch record a start/stop event
+ * pair on its stream; echo_profile_read() waits for the recorded events, fills
+ * up to `max` entries (kernel name, number of launches, summed milliseconds)
+ * and clears the record.  Returns the number of entries written, or a negative
+ * echo_status on failure.  Enabling adds two event records per launch.
+ */
+typedef struct {
+  const char* name;
+  int64_t launches;
+  double total_ms;
+} echo_kernel_time;
+
+int echo_profile_enable(int on);
+int echo_profile_read(echo_kernel_time* out, int32_t max);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ECHO_H */

@@ -1,0 +1,287 @@
+"""Python binding of libecho: the four calls of one cached DiT block step on
+torch device tensors.
+
+Argument marshalling only: torch provides device memory (outputs and
+workspaces are torch tensors) and the stream (the current torch stream); every
+step of the path runs in the library's HIP kernels.
+
+  energy(audio, T)                       audio energy anchor, once per clip
+  select(x, xref, frame_weight, N, k)    saliency + top-K / threshold selection
+  block_partial(w, x, idx, n_sel, H)     DiT block on the selected tokens
+  cache_update(x, idx, mask, n_sel, ...) int8 residual cache write + reuse
+  CachedBlock                            the four calls composed, with its cache
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+
+import torch
+
+from . import _lib
+from ._lib import (BlockCfg, BlockWeights, CacheCfg, EnergyCfg, KernelTime, SelectCfg,
+                   ECHO_BF16, ECHO_F32, check)
+
+_DTYPES = {torch.float32: ECHO_F32, torch.bfloat16: ECHO_BF16}
+
+
+def _lib_handle():
+    return _lib.load()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t
+
+
+def _echo_dtype(t: torch.Tensor) -> int:
+    if t.dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return _DTYPES[t.dtype]
+
+
+class Workspace:
+    """A growable device byte buffer reused across calls."""
+
+    def __init__(self):
+        self.buf = None
+
+    def get(self, nbytes: int, device) -> torch.Tensor:
+        nbytes = max(int(nbytes), 256)
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != device:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        return self.buf
+
+
+_WS = {"energy": Workspace(), "select": Workspace(), "block": Workspace()}
+
+
+# --------------------------------------------------------------------- energy
+
+def energy_cfg(T, sample_rate=16000, n_fft=512, hop=160, n_bands=8) -> EnergyCfg:
+    return EnergyCfg(T, sample_rate, n_fft, hop, n_bands)
+
+
+def energy(audio: torch.Tensor, T: int, sample_rate: int = 16000, n_fft: int = 512,
+           hop: int = 160, n_bands: int = 8, workspace: Workspace | None = None):
+    """(band_energy [T, n_bands], frame_energy [T], frame_weight [T]), fp32."""
+    lib = _lib_handle()
+    _dev(audio, "audio", torch.float32)
+    cfg = energy_cfg(T, sample_rate, n_fft, hop, n_bands)
+    n = audio.numel()
+    dev = audio.device
+    band = torch.empty((T, n_bands), dtype=torch.float32, device=dev)
+    fe = torch.empty(T, dtype=torch.float32, device=dev)
+    fw = torch.empty(T, dtype=torch.float32, device=dev)
+    need = lib.echo_energy_workspace(ctypes.byref(cfg), n)
+    if need == 0:
+        check("echo_energy", _lib.ECHO_EINVAL)
+    ws = (workspace or _WS["energy"]).get(need, dev)
+    check("echo_energy", lib.echo_energy(ctypes.byref(cfg), _ptr(audio), n, _ptr(band), _ptr(fe),
+                                         _ptr(fw), _ptr(ws), ws.numel(), _stream()))
+    return band, fe, fw
+
+
+# --------------------------------------------------------------------- select
+
+@dataclasses.dataclass
+class Selection:
+    idx: torch.Tensor          # int32 [L]; the first n_sel entries are valid, ascending
+    mask: torch.Tensor         # uint8 [L]
+    n_sel_dev: torch.Tensor    # int32 [1] on the device
+    n_sel: int | None          # known on the host in top-k mode
+    saliency: torch.Tensor | None
+    step_delta: torch.Tensor | None
+
+    def count(self) -> int:
+        return self.n_sel if self.n_sel is not None else int(self.n_sel_dev.item())
+
+    def indices(self) -> torch.Tensor:
+        return self.idx[: self.count()]
+
+
+def select(x: torch.Tensor, xref: torch.Tensor, frame_weight: torch.Tensor, N: int,
+           k: int | None = None, threshold: float | None = None, xi: float = 1e-6,
+           want_saliency: bool = True, want_step_delta: bool = True,
+           out: Selection | None = None, workspace: Workspace | None = None) -> Selection:
+    """Saliency and selection; pass k for top-k mode or threshold for threshold mode."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    _dev(xref, "xref", x.dtype)
+    _dev(frame_weight, "frame_weight", torch.float32)
+    L, D = x.shape
+    if L % N:
+        raise ValueError("L must be a multiple of N")
+    T = L // N
+    if (k is None) == (threshold is None):
+        raise ValueError("pass exactly one of k and threshold")
+    cfg = SelectCfg(T, N, D, _echo_dtype(x), -1 if k is None else int(k),
+                    0.0 if threshold is None else float(threshold), float(xi))
+    dev = x.device
+    if out is None:
+        out = Selection(
+            idx=torch.empty(L, dtype=torch.int32, device=dev),
+            mask=torch.empty(L, dtype=torch.uint8, device=dev),
+            n_sel_dev=torch.empty(1, dtype=torch.int32, device=dev),
+            n_sel=None,
+            saliency=torch.empty(L, dtype=torch.float32, device=dev) if want_saliency else None,
+            step_delta=torch.empty(1, dtype=torch.float64, device=dev) if want_step_delta else None)
+    out.n_sel = None if k is None else int(k)
+    need = lib.echo_select_workspace(ctypes.byref(cfg))
+    if need == 0:
+        check("echo_select", _lib.ECHO_EINVAL)
+    ws = (workspace or _WS["select"]).get(need, dev)
+    check("echo_select", lib.echo_select(ctypes.byref(cfg), _ptr(x), _ptr(xref), _ptr(frame_weight),
+                                         _ptr(out.idx), _ptr(out.mask), _ptr(out.n_sel_dev),
+                                         _ptr(out.saliency), _ptr(out.step_delta), _ptr(ws),
+                                         ws.numel(), _stream()))
+    return out
+
+
+def topk_count(ratio: float, L: int) -> int:
+    """K = ceil(r L), clamped to [0, L]; the small offset keeps exact products
+    such as 0.4 * 32760 from rounding up."""
+    return min(L, max(0, math.ceil(ratio * L - 1e-9)))
+
+
+# ------------------------------------------------------------- block partial
+
+WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "w1", "w2", "bq", "bk", "bv", "bo", "b1", "b2", "mod")
+
+
+def block_weights(params: dict) -> BlockWeights:
+    for n in WEIGHT_NAMES:
+        _dev(params[n], n)
+    return BlockWeights(*[params[n].data_ptr() for n in WEIGHT_NAMES])
+
+
+def block_partial(params: dict, x: torch.Tensor, idx: torch.Tensor, n_sel: int, H: int,
+                  ln_eps: float = 1e-6, y_sel: torch.Tensor | None = None,
+                  workspace: Workspace | None = None, _weights: BlockWeights | None = None):
+    """y_sel [n_sel, D] fp32 = block output of tokens idx[:n_sel]."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    _dev(idx, "idx", torch.int32)
+    L, D = x.shape
+    F = params["w1"].shape[0]
+    for n in WEIGHT_NAMES[:-1]:
+        if params[n].dtype != x.dtype:
+            raise TypeError(f"{n} must have the activation dtype {x.dtype}")
+    _dev(params["mod"], "mod", torch.float32)
+    cfg = BlockCfg(L, D, H, F, _echo_dtype(x), float(ln_eps))
+    w = _weights if _weights is not None else block_weights(params)
+    if y_sel is None:
+        y_sel = torch.empty((max(n_sel, 1), D), dtype=torch.float32, device=x.device)
+    if n_sel == 0:
+        return y_sel[:0]
+    need = lib.echo_block_workspace(ctypes.byref(cfg), n_sel)
+    if need == 0:
+        check("echo_block_partial", _lib.ECHO_EINVAL)
+    ws = (workspace or _WS["block"]).get(need, x.device)
+    check("echo_block_partial",
+          lib.echo_block_partial(ctypes.byref(cfg), ctypes.byref(w), _ptr(x), _ptr(idx), n_sel,
+                                 _ptr(y_sel), _ptr(ws), ws.numel(), _stream()))
+    return y_sel[:n_sel]
+
+
+# --------------------------------------------------------------- cache update
+
+def cache_update(x: torch.Tensor, idx: torch.Tensor, mask: torch.Tensor, n_sel: int,
+                 y_sel: torch.Tensor, xref: torch.Tensor, codes: torch.Tensor,
+                 scale: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+    """Writes the fresh rows into (xref, codes, scale) in place; returns y."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    L, D = x.shape
+    _dev(mask, "mask", torch.uint8)
+    _dev(xref, "xref", x.dtype)
+    _dev(codes, "codes", torch.int8)
+    _dev(scale, "scale", torch.float32)
+    if n_sel > 0:
+        _dev(idx, "idx", torch.int32)
+        _dev(y_sel, "y_sel", torch.float32)
+    if y is None:
+        y = torch.empty_like(x)
+    cfg = CacheCfg(L, D, _echo_dtype(x))
+    check("echo_cache_update",
+          lib.echo_cache_update(ctypes.byref(cfg), _ptr(x), _ptr(idx) if n_sel else None,
+                                _ptr(mask), n_sel, _ptr(y_sel) if n_sel else None, _ptr(xref),
+                                _ptr(codes), _ptr(scale), _ptr(y), _stream()))
+    return y
+
+
+# ------------------------------------------------------------- kernel timing
+
+def profile_enable(on: bool = True) -> None:
+    check("echo_profile_enable", _lib_handle().echo_profile_enable(1 if on else 0))
+
+
+def profile_read(max_entries: int = 64) -> dict:
+    """{kernel name: (launches, total ms)} for launches since the last read."""
+    lib = _lib_handle()
+    arr = (KernelTime * max_entries)()
+    n = lib.echo_profile_read(arr, max_entries)
+    if n < 0:
+        check("echo_profile_read", -n)
+    return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms)) for i in range(n)}
+
+
+# ---------------------------------------------------------------- composition
+
+class CachedBlock:
+    """One DiT block with an EchoCache int8 residual cache on one device.
+
+    init(x)                 recompute every token and fill the cache (first step)
+    step(x, w, ratio|k)     saliency -> top-K -> partial block -> cache update
+    Returns the block output y [L, D] in the activation dtype.
+    """
+
+    def __init__(self, params: dict, H: int, L: int, D: int, device, dtype,
+                 ln_eps: float = 1e-6, xi: float = 1e-6):
+        self.params = params
+        self.H, self.L, self.D = H, L, D
+        self.ln_eps, self.xi = ln_eps, xi
+        self.xref = torch.zeros((L, D), dtype=dtype, device=device)
+        self.codes = torch.zeros((L, D), dtype=torch.int8, device=device)
+        self.scale = torch.zeros(L, dtype=torch.float32, device=device)
+        self.y = torch.empty((L, D), dtype=dtype, device=device)
+        self.y_sel = torch.empty((L, D), dtype=torch.float32, device=device)
+        self.all_idx = torch.arange(L, dtype=torch.int32, device=device)
+        self.all_mask = torch.ones(L, dtype=torch.uint8, device=device)
+        self.ws = Workspace()
+        self.sel_ws = Workspace()
+        self.sel = None
+        self._w = block_weights(params)
+
+    def init(self, x: torch.Tensor) -> torch.Tensor:
+        ys = block_partial(self.params, x, self.all_idx, self.L, self.H, self.ln_eps,
+                           y_sel=self.y_sel, workspace=self.ws, _weights=self._w)
+        return cache_update(x, self.all_idx, self.all_mask, self.L, ys, self.xref, self.codes,
+                            self.scale, self.y)
+
+    def step(self, x: torch.Tensor, frame_weight: torch.Tensor, N: int,
+             ratio: float | None = None, k: int | None = None) -> torch.Tensor:
+        if k is None:
+            k = topk_count(ratio, self.L)
+        self.sel = select(x, self.xref, frame_weight, N, k=k, xi=self.xi, out=self.sel,
+                          workspace=self.sel_ws)
+        ys = block_partial(self.params, x, self.sel.idx, k, self.H, self.ln_eps,
+                           y_sel=self.y_sel, workspace=self.ws, _weights=self._w)
+        return cache_update(x, self.sel.idx, self.sel.mask, k, ys, self.xref, self.codes,
+                            self.scale, self.y)

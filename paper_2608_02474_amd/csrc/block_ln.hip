@@ -1,0 +1,156 @@
+// Modulated LayerNorm of token rows (the adaLN "LN(z) * (1 + scale) + shift"
+// in front of attention and FFN of the DiT block, Sec. 3.3).
+//
+// One wave per row; the row is held in registers (8-element chunks), mean and
+// biased variance are reduced in fp32 with two passes over the registers, and
+// the modulated result is written in the output storage type.  Rows longer than
+// 512 * MAXC elements take the MAXC == 0 variant, which re-reads the row.
+#include "common.h"
+#include "kernels.h"
+#include "launch.h"
+
+namespace echo {
+
+constexpr int kLnThreads = 256;
+constexpr int kLnWaves = kLnThreads / kWave;
+
+__device__ __forceinline__ void ln_load8(const float* p, float* v) {
+  unpack16(ldg16(p), v, static_cast<const float*>(nullptr));
+  unpack16(ldg16(p + 4), v + 4, static_cast<const float*>(nullptr));
+}
+__device__ __forceinline__ void ln_load8(const bf16_t* p, float* v) {
+  unpack16(ldg16(p), v, static_cast<const bf16_t*>(nullptr));
+}
+__device__ __forceinline__ void ln_store8(float* p, const float* v) {
+  stg16(p, pack16(v, static_cast<const float*>(nullptr)));
+  stg16(p + 4, pack16(v + 4, static_cast<const float*>(nullptr)));
+}
+__device__ __forceinline__ void ln_store8(bf16_t* p, const float* v) {
+  stg16(p, pack16(v, static_cast<const bf16_t*>(nullptr)));
+}
+
+template <typename Tin, typename Tout, int MAXC>
+__global__ void __launch_bounds__(kLnThreads)
+modln_rows(const Tin* __restrict__ x, int M, int D, const float* __restrict__ shift,
+           const float* __restrict__ scale, float eps, Tout* __restrict__ out) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kLnWaves + wave;
+  if (row >= M) return;
+  const Tin* xr = x + row * D;
+  Tout* orow = out + row * D;
+  const int nch = D / 8;
+  const float invD = 1.0f / static_cast<float>(D);
+  if (MAXC > 0) {
+    constexpr int R = MAXC > 0 ? MAXC : 1;
+    float v[R][8];
+    float sum = 0.0f;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int c = lane + u * kWave;
+      if (c < nch) {
+        ln_load8(xr + c * 8, v[u]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sum += v[u][j];
+      }
+    }
+    const float mean = wave_sum(sum) * invD;
+    float sq = 0.0f;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int c = lane + u * kWave;
+      if (c < nch) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float d = v[u][j] - mean;
+          sq += d * d;
+        }
+      }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(sq) * invD + eps);
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int c = lane + u * kWave;
+      if (c < nch) {
+        float o[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int col = c * 8 + j;
+          o[j] = (v[u][j] - mean) * rstd * (1.0f + scale[col]) + shift[col];
+        }
+        ln_store8(orow + c * 8, o);
+      }
+    }
+  } else {
+    float sum = 0.0f;
+    for (int c = lane; c < nch; c += kWave) {
+      float v[8];
+      ln_load8(xr + c * 8, v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sum += v[j];
+    }
+    const float mean = wave_sum(sum) * invD;
+    float sq = 0.0f;
+    for (int c = lane; c < nch; c += kWave) {
+      float v[8];
+      ln_load8(xr + c * 8, v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float d = v[j] - mean;
+        sq += d * d;
+      }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(sq) * invD + eps);
+    for (int c = lane; c < nch; c += kWave) {
+      float v[8], o[8];
+      ln_load8(xr + c * 8, v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int col = c * 8 + j;
+        o[j] = (v[j] - mean) * rstd * (1.0f + scale[col]) + shift[col];
+      }
+      ln_store8(orow + c * 8, o);
+    }
+  }
+}
+
+template <typename Tin, typename Tout>
+static hipError_t launch_modln_t(const char* name, const Tin* x, int M, int D, const float* shift,
+                                 const float* scale, float eps, Tout* out, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  const dim3 grid((M + kLnWaves - 1) / kLnWaves);
+  const int per_lane = (D / 8 + kWave - 1) / kWave;
+#define ECHO_LN_CASE(MC)                                                                       \
+  if (per_lane <= MC)                                                                          \
+    return ECHO_LAUNCH(name, (modln_rows<Tin, Tout, MC>), grid, dim3(kLnThreads), 0, stream, x, \
+                       M, D, shift, scale, eps, out);
+  ECHO_LN_CASE(2)
+  ECHO_LN_CASE(4)
+  ECHO_LN_CASE(8)
+  ECHO_LN_CASE(12)
+  ECHO_LN_CASE(16)
+#undef ECHO_LN_CASE
+  return ECHO_LAUNCH(name, (modln_rows<Tin, Tout, 0>), grid, dim3(kLnThreads), 0, stream, x, M, D,
+                     shift, scale, eps, out);
+}
+
+// LN1 over the block input rows (bf16 -> bf16, or f32 -> f32).
+hipError_t launch_modln_input(int dtype_bf16, const void* x, int M, int D, const float* shift,
+                              const float* scale, float eps, void* out, hipStream_t stream) {
+  if (dtype_bf16)
+    return launch_modln_t<bf16_t, bf16_t>("modln_in_bf16", static_cast<const bf16_t*>(x), M, D, shift,
+                                          scale, eps, static_cast<bf16_t*>(out), stream);
+  return launch_modln_t<float, float>("modln_in_f32", static_cast<const float*>(x), M, D, shift, scale,
+                                      eps, static_cast<float*>(out), stream);
+}
+
+// LN2 over the fp32 attention-residual rows x1 (-> bf16 or f32).
+hipError_t launch_modln_x1(int dtype_bf16, const float* x1, int M, int D, const float* shift,
+                           const float* scale, float eps, void* out, hipStream_t stream) {
+  if (dtype_bf16)
+    return launch_modln_t<float, bf16_t>("modln_x1_bf16", x1, M, D, shift, scale, eps,
+                                         static_cast<bf16_t*>(out), stream);
+  return launch_modln_t<float, float>("modln_x1_f32", x1, M, D, shift, scale, eps,
+                                      static_cast<float*>(out), stream);
+}
+
+}  // namespace echo

@@ -1,0 +1,184 @@
+// Int8 residual cache write and mask fusion (Sec. 3.3: output = m * fresh +
+// (1 - m) * cached; Sec. 3.4: cached = reference + dequantized int8 residual,
+// cast back to the compute precision).
+//
+// One launch, one wave per row:
+//   waves [0, n_sel)        recomputed row i = idx[j]: res = y_sel[j] - x_i in
+//                           fp32, absmax, per-row scale, int8 codes, reference
+//                           := x_i, output := cast(y_sel[j]);
+//   waves [n_sel, n_sel+L)  row i = wave - n_sel, if mask[i] == 0: output :=
+//                           cast(xref_i + scale_i * code).
+// Rows are streamed with 16-byte loads/stores (8 elements per chunk); the
+// fresh row is held in registers between the absmax and the quantization.
+// Every fp32 step is a separately rounded IEEE operation (no fused
+// multiply-add), so codes and reused rows are exactly the fp32 values the
+// definition gives.
+#include "common.h"
+#include "kernels.h"
+#include "launch.h"
+
+namespace echo {
+
+constexpr int kCacheThreads = 256;
+constexpr int kCacheWavesPerBlock = kCacheThreads / kWave;
+
+__device__ __forceinline__ void load8(const float* p, float* v) {
+  const uint4 a = ldg16(p), b = ldg16(p + 4);
+  unpack16(a, v, static_cast<const float*>(nullptr));
+  unpack16(b, v + 4, static_cast<const float*>(nullptr));
+}
+__device__ __forceinline__ void load8(const bf16_t* p, float* v) {
+  unpack16(ldg16(p), v, static_cast<const bf16_t*>(nullptr));
+}
+__device__ __forceinline__ void store8(float* p, const float* v) {
+  stg16(p, pack16(v, static_cast<const float*>(nullptr)));
+  stg16(p + 4, pack16(v + 4, static_cast<const float*>(nullptr)));
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float* v) {
+  stg16(p, pack16(v, static_cast<const bf16_t*>(nullptr)));
+}
+__device__ __forceinline__ void copy8(const float* src, float* dst) {
+  stg16(dst, ldg16(src));
+  stg16(dst + 4, ldg16(src + 4));
+}
+__device__ __forceinline__ void copy8(const bf16_t* src, bf16_t* dst) { stg16(dst, ldg16(src)); }
+
+// fp32(fp32(a * b) + c): multiply and add rounded separately, never fused.
+__device__ __forceinline__ float mul_add_unfused(float a, float b, float c) {
+#pragma clang fp contract(off)
+  return a * b + c;
+}
+
+// Quantize one 8-element chunk of a fresh row and store its codes.
+__device__ __forceinline__ void quantize8(const float* res, float inv, int8_t* dst) {
+  uint32_t w[2] = {0u, 0u};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    float q = rintf(__fmul_rn(res[j], inv));
+    q = fminf(fmaxf(q, -127.0f), 127.0f);
+    const uint32_t b = static_cast<uint32_t>(static_cast<int32_t>(q)) & 0xffu;
+    w[j / 4] |= b << (8 * (j % 4));
+  }
+  *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+}
+
+// MAXC > 0: the fresh row's residual stays in registers (D <= 512 * MAXC);
+// MAXC == 0: the row is streamed twice (any D).
+template <typename T, int MAXC>
+__global__ void __launch_bounds__(kCacheThreads)
+cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
+                  const uint8_t* __restrict__ mask, int n_sel, int L, int D,
+                  const float* __restrict__ y_sel, T* __restrict__ xref, int8_t* __restrict__ codes,
+                  float* __restrict__ scale, T* __restrict__ y) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kCacheWavesPerBlock + wave;
+  const int nch = D / 8;
+  if (g < n_sel) {
+    const int64_t i = idx[g];
+    const float* ys = y_sel + g * D;
+    const T* xi = x + i * D;
+    constexpr int R = MAXC > 0 ? MAXC : 1;
+    float res[R][8];
+    float amax = 0.0f;
+    if (MAXC > 0) {
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        if (c < nch) {
+          float yv[8], xv[8];
+          load8(ys + c * 8, yv);
+          load8(xi + c * 8, xv);
+          store8(y + i * D + c * 8, yv);           // fresh output, cast to storage type
+          copy8(xi + c * 8, xref + i * D + c * 8);  // reference := current input
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            res[u][j] = __fsub_rn(yv[j], xv[j]);
+            amax = fmaxf(amax, fabsf(res[u][j]));
+          }
+        }
+      }
+    } else {
+      for (int c = lane; c < nch; c += kWave) {
+        float yv[8], xv[8];
+        load8(ys + c * 8, yv);
+        load8(xi + c * 8, xv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(__fsub_rn(yv[j], xv[j])));
+      }
+    }
+    amax = wave_max(amax);
+    const bool nz = amax > 0.0f;
+    const float inv = nz ? __fdiv_rn(127.0f, amax) : 0.0f;
+    if (lane == 0) scale[i] = nz ? __fdiv_rn(amax, 127.0f) : 0.0f;
+    if (MAXC > 0) {
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        if (c < nch) quantize8(res[u], inv, codes + i * D + c * 8);
+      }
+    } else {
+      for (int c = lane; c < nch; c += kWave) {
+        float yv[8], xv[8], r[8];
+        load8(ys + c * 8, yv);
+        load8(xi + c * 8, xv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) r[j] = __fsub_rn(yv[j], xv[j]);
+        quantize8(r, inv, codes + i * D + c * 8);
+        store8(y + i * D + c * 8, yv);
+        copy8(xi + c * 8, xref + i * D + c * 8);
+      }
+    }
+    return;
+  }
+  const int64_t i = g - n_sel;
+  if (i >= L || mask[i]) return;
+  const float sc = scale[i];
+  for (int c = lane; c < nch; c += kWave) {
+    float r[8];
+    load8(xref + i * D + c * 8, r);
+    const uint2 cw = *reinterpret_cast<const uint2*>(codes + i * D + c * 8);
+    const uint32_t w[2] = {cw.x, cw.y};
+    float out[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int8_t q = static_cast<int8_t>((w[j / 4] >> (8 * (j % 4))) & 0xffu);
+      out[j] = mul_add_unfused(sc, static_cast<float>(q), r[j]);
+    }
+    store8(y + i * D + c * 8, out);
+  }
+}
+
+template <typename T>
+static hipError_t launch_cache_t(const char* name, const T* x, const int32_t* idx, const uint8_t* mask,
+                                 int n_sel, int L, int D, const float* y_sel, T* xref, int8_t* codes,
+                                 float* scale, T* y, hipStream_t stream) {
+  const int64_t waves = static_cast<int64_t>(n_sel) + L;
+  const dim3 grid(static_cast<unsigned>((waves + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
+  const int per_lane = (D / 8 + kWave - 1) / kWave;
+#define ECHO_CACHE_CASE(MC)                                                                    \
+  if (per_lane <= MC)                                                                          \
+    return ECHO_LAUNCH(name, (cache_update_rows<T, MC>), grid, dim3(kCacheThreads), 0, stream, \
+                       x, idx, mask, n_sel, L, D, y_sel, xref, codes, scale, y);
+  ECHO_CACHE_CASE(2)
+  ECHO_CACHE_CASE(4)
+  ECHO_CACHE_CASE(8)
+  ECHO_CACHE_CASE(12)
+  ECHO_CACHE_CASE(16)
+#undef ECHO_CACHE_CASE
+  return ECHO_LAUNCH(name, (cache_update_rows<T, 0>), grid, dim3(kCacheThreads), 0, stream, x, idx,
+                     mask, n_sel, L, D, y_sel, xref, codes, scale, y);
+}
+
+hipError_t launch_cache_update(int dtype_bf16, const void* x, const int32_t* idx, const uint8_t* mask,
+                               int n_sel, int L, int D, const float* y_sel, void* xref, int8_t* codes,
+                               float* scale, void* y, hipStream_t stream) {
+  if (dtype_bf16)
+    return launch_cache_t<bf16_t>("cache_update_bf16", static_cast<const bf16_t*>(x), idx, mask, n_sel,
+                                  L, D, y_sel, static_cast<bf16_t*>(xref), codes, scale,
+                                  static_cast<bf16_t*>(y), stream);
+  return launch_cache_t<float>("cache_update_f32", static_cast<const float*>(x), idx, mask, n_sel, L,
+                               D, y_sel, static_cast<float*>(xref), codes, scale,
+                               static_cast<float*>(y), stream);
+}
+
+}  // namespace echo

@@ -1,0 +1,94 @@
+// Shared device helpers for the gfx950 kernels: storage types, bf16 rounding,
+// 16-byte vector access and wave64 reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace echo {
+
+typedef uint16_t bf16_t;                                            // storage
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));         // MFMA operand
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest even; NaN stays NaN (quiet).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+// Element loads/stores that hide the storage type.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static constexpr int kPerVec = 4;  // elements per 16 bytes
+  __device__ static float load(const float* p, int64_t i) { return p[i]; }
+  __device__ static void store(float* p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<bf16_t> {
+  static constexpr int kPerVec = 8;
+  __device__ static float load(const bf16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+  __device__ static void store(bf16_t* p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+// 16-byte vector of 8 bf16 or 4 fp32 unpacked to fp32.
+__device__ __forceinline__ void unpack16(const uint4& v, float* out, const bf16_t*) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    out[2 * j] = __uint_as_float(w[j] << 16);
+    out[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void unpack16(const uint4& v, float* out, const float*) {
+  out[0] = __uint_as_float(v.x);
+  out[1] = __uint_as_float(v.y);
+  out[2] = __uint_as_float(v.z);
+  out[3] = __uint_as_float(v.w);
+}
+__device__ __forceinline__ uint4 pack16(const float* in, const bf16_t*) {
+  uint4 v;
+  v.x = f32_to_bf16(in[0]) | (static_cast<uint32_t>(f32_to_bf16(in[1])) << 16);
+  v.y = f32_to_bf16(in[2]) | (static_cast<uint32_t>(f32_to_bf16(in[3])) << 16);
+  v.z = f32_to_bf16(in[4]) | (static_cast<uint32_t>(f32_to_bf16(in[5])) << 16);
+  v.w = f32_to_bf16(in[6]) | (static_cast<uint32_t>(f32_to_bf16(in[7])) << 16);
+  return v;
+}
+__device__ __forceinline__ uint4 pack16(const float* in, const float*) {
+  return make_uint4(__float_as_uint(in[0]), __float_as_uint(in[1]), __float_as_uint(in[2]),
+                    __float_as_uint(in[3]));
+}
+
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ void stg16(void* p, const uint4& v) {
+  *reinterpret_cast<uint4*>(p) = v;
+}
+
+// wave64 reductions (every lane gets the result)
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+}  // namespace echo

@@ -1,0 +1,359 @@
+// C ABI of libecho: argument validation, workspace carving and the launch
+// sequence of each call.  Every check runs before the first HIP call, so a
+// rejected call touches neither the device nor the stream.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+
+#include <vector>
+
+#include "../../include/echo.h"
+#include "kernels.h"
+#include "launch.h"
+
+namespace echo {
+
+// ---- per-thread error and timing state
+static thread_local int g_last_hip_error = 0;
+
+struct TimingRecord {
+  const char* name;
+  hipEvent_t start, stop;
+};
+static thread_local bool g_profile = false;
+static thread_local std::vector<TimingRecord> g_records;
+static thread_local std::vector<hipEvent_t> g_event_pool;
+
+bool profile_enabled() { return g_profile; }
+void profile_set(bool on) { g_profile = on; }
+
+static hipEvent_t take_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+TimedLaunch::TimedLaunch(const char* name, hipStream_t s) : slot(-1), stream(s) {
+  if (!g_profile) return;
+  TimingRecord r{name, take_event(), take_event()};
+  if (r.start == nullptr || r.stop == nullptr || hipEventRecord(r.start, s) != hipSuccess) {
+    if (r.start) g_event_pool.push_back(r.start);
+    if (r.stop) g_event_pool.push_back(r.stop);
+    return;
+  }
+  g_records.push_back(r);
+  slot = static_cast<int>(g_records.size()) - 1;
+}
+TimedLaunch::~TimedLaunch() {
+  if (slot >= 0) (void)hipEventRecord(g_records[slot].stop, stream);
+}
+
+}  // namespace echo
+
+using namespace echo;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool ok_ptr(const void* p) { return p != nullptr && aligned16(p); }
+inline size_t esize(int dtype) { return dtype == ECHO_BF16 ? 2 : 4; }
+inline bool ok_dtype(int dtype) { return dtype == ECHO_F32 || dtype == ECHO_BF16; }
+
+int device_status(hipError_t e) {
+  if (e == hipSuccess) return ECHO_OK;
+  g_last_hip_error = static_cast<int>(e);
+  return ECHO_EDEVICE;
+}
+
+// ---- energy
+bool energy_cfg_ok(const echo_energy_cfg* c, int64_t n_samples) {
+  return c != nullptr && c->T >= 1 && c->T <= 65535 && n_samples >= c->T && c->n_fft >= 16 &&
+         c->n_fft <= 2048 && (c->n_fft % 2) == 0 && c->hop >= 1 && c->n_bands >= 1 &&
+         c->n_bands <= 64 && c->sample_rate > 0;
+}
+size_t energy_ws(const echo_energy_cfg* c, int64_t n_samples) {
+  const int mf = energy_max_frames(n_samples, c->T, c->n_fft, c->hop);
+  return align_up(sizeof(double) * static_cast<size_t>(c->T) * mf * c->n_bands) +
+         align_up(sizeof(double) * static_cast<size_t>(c->T));
+}
+
+// ---- select
+bool select_cfg_ok(const echo_select_cfg* c) {
+  if (c == nullptr || c->T < 1 || c->N < 1 || c->D < 8 || (c->D % 8) != 0 || !ok_dtype(c->dtype))
+    return false;
+  const int64_t L = static_cast<int64_t>(c->T) * c->N;
+  if (L >= (int64_t(1) << 31)) return false;
+  if (c->k > L) return false;
+  if (!(c->xi >= 0.0) || isnan(c->threshold)) return false;
+  return true;
+}
+size_t select_ws(const echo_select_cfg* c) {
+  const size_t L = static_cast<size_t>(c->T) * c->N;
+  return align_up(L * sizeof(float)) + 2 * align_up(L * sizeof(double));
+}
+
+// ---- block
+bool block_cfg_ok(const echo_block_cfg* c) {
+  return c != nullptr && c->L >= 1 && c->D >= 8 && c->H >= 1 && c->F >= 8 && ok_dtype(c->dtype) &&
+         c->D <= 16384 && c->F <= 65536 && (c->D % c->H) == 0 && (c->D % 8) == 0 &&
+         (c->F % 8) == 0 && c->ln_eps >= 0.0f;
+}
+bool block_supported(const echo_block_cfg* c) {
+  const int dh = c->D / c->H;
+  if (c->dtype == ECHO_BF16) return dh == 128 && (c->D % 256) == 0 && (c->F % 256) == 0;
+  return dh <= 128;
+}
+struct BlockWs {
+  void *a, *kv, *q, *o, *b, *h;
+  float* x1;
+  size_t bytes;
+};
+BlockWs block_ws_layout(const echo_block_cfg* c, int64_t n, char* base) {
+  const size_t es = esize(c->dtype);
+  const size_t L = c->L, D = c->D, F = c->F, m = static_cast<size_t>(n);
+  BlockWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* p = base ? base + off : nullptr;
+    off += align_up(bytes);
+    return p;
+  };
+  w.a = take(L * D * es);
+  w.kv = take(L * 2 * D * es);
+  w.q = take(m * D * es);
+  w.o = take(m * D * es);
+  w.x1 = reinterpret_cast<float*>(take(m * D * 4));
+  w.b = take(m * D * es);
+  w.h = take(m * F * es);
+  w.bytes = off;
+  return w;
+}
+bool weights_ok(const echo_block_weights* w) {
+  return w != nullptr && ok_ptr(w->wq) && ok_ptr(w->wk) && ok_ptr(w->wv) && ok_ptr(w->wo) &&
+         ok_ptr(w->w1) && ok_ptr(w->w2) && ok_ptr(w->bq) && ok_ptr(w->bk) && ok_ptr(w->bv) &&
+         ok_ptr(w->bo) && ok_ptr(w->b1) && ok_ptr(w->b2) && ok_ptr(w->mod);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* echo_status_str(int status) {
+  switch (status) {
+    case ECHO_OK: return "ok";
+    case ECHO_EINVAL: return "invalid argument";
+    case ECHO_EUNSUPPORTED: return "unsupported shape or dtype";
+    case ECHO_EWORKSPACE: return "workspace missing or too small";
+    case ECHO_EDEVICE: return "HIP device error";
+    default: return "unknown status";
+  }
+}
+
+int echo_last_hip_error(void) { return g_last_hip_error; }
+
+const char* echo_version(void) { return "0.1.0"; }
+
+size_t echo_energy_workspace(const echo_energy_cfg* cfg, int64_t n_samples) {
+  if (!energy_cfg_ok(cfg, n_samples)) return 0;
+  return energy_ws(cfg, n_samples);
+}
+
+int echo_energy(const echo_energy_cfg* cfg, const float* audio, int64_t n_samples, float* band_energy,
+                float* frame_energy, float* frame_weight, void* workspace, size_t workspace_bytes,
+                void* stream) {
+  if (!energy_cfg_ok(cfg, n_samples)) return ECHO_EINVAL;
+  if (!ok_ptr(audio) || !ok_ptr(band_energy) || !ok_ptr(frame_energy) || !ok_ptr(frame_weight))
+    return ECHO_EINVAL;
+  const size_t need = energy_ws(cfg, n_samples);
+  if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
+  const int mf = energy_max_frames(n_samples, cfg->T, cfg->n_fft, cfg->hop);
+  double* part = static_cast<double*>(workspace);
+  double* e_scr = reinterpret_cast<double*>(
+      static_cast<char*>(workspace) +
+      align_up(sizeof(double) * static_cast<size_t>(cfg->T) * mf * cfg->n_bands));
+  return device_status(launch_energy(audio, n_samples, cfg->T, cfg->sample_rate, cfg->n_fft, cfg->hop,
+                                     cfg->n_bands, band_energy, frame_energy, frame_weight, part,
+                                     e_scr, static_cast<hipStream_t>(stream)));
+}
+
+size_t echo_select_workspace(const echo_select_cfg* cfg) {
+  if (!select_cfg_ok(cfg)) return 0;
+  return select_ws(cfg);
+}
+
+int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
+                int32_t* idx, uint8_t* mask, int32_t* n_sel, float* saliency, double* step_delta,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  if (!select_cfg_ok(cfg)) return ECHO_EINVAL;
+  if (!ok_ptr(x) || !ok_ptr(xref) || !ok_ptr(frame_weight) || !ok_ptr(idx) || !ok_ptr(mask) ||
+      n_sel == nullptr)
+    return ECHO_EINVAL;
+  if ((saliency != nullptr && !aligned16(saliency)) ||
+      (step_delta != nullptr && (reinterpret_cast<uintptr_t>(step_delta) & 7u)))
+    return ECHO_EINVAL;
+  const size_t need = select_ws(cfg);
+  if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
+  const int L = cfg->T * cfg->N;
+  char* ws = static_cast<char*>(workspace);
+  float* s_ws = reinterpret_cast<float*>(ws);
+  double* num = reinterpret_cast<double*>(ws + align_up(L * sizeof(float)));
+  double* den = reinterpret_cast<double*>(ws + align_up(L * sizeof(float)) + align_up(L * sizeof(double)));
+  float* s = saliency ? saliency : s_ws;
+  const int threshold_mode = cfg->k < 0 ? 1 : 0;
+  return device_status(launch_select(cfg->dtype == ECHO_BF16, x, xref, frame_weight, L, cfg->N, cfg->D,
+                                     cfg->xi, threshold_mode ? 0 : cfg->k, threshold_mode,
+                                     cfg->threshold, s, num, den, idx, mask, n_sel, step_delta,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+size_t echo_block_workspace(const echo_block_cfg* cfg, int32_t n_sel_max) {
+  if (!block_cfg_ok(cfg) || n_sel_max < 0) return 0;
+  return block_ws_layout(cfg, n_sel_max, nullptr).bytes;
+}
+
+int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, const void* x,
+                       const int32_t* idx, int32_t n_sel, float* y_sel, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  if (!block_cfg_ok(cfg) || !weights_ok(w) || n_sel < 0) return ECHO_EINVAL;
+  if (!block_supported(cfg)) return ECHO_EUNSUPPORTED;
+  if (n_sel == 0) return ECHO_OK;
+  if (!ok_ptr(x) || !ok_ptr(idx) || !ok_ptr(y_sel)) return ECHO_EINVAL;
+  const size_t need = block_ws_layout(cfg, n_sel, nullptr).bytes;
+  if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
+  const BlockWs ws = block_ws_layout(cfg, n_sel, static_cast<char*>(workspace));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int L = cfg->L, D = cfg->D, H = cfg->H, F = cfg->F, n = n_sel;
+  const float* mod = w->mod;
+  const bool bf = cfg->dtype == ECHO_BF16;
+  hipError_t e = launch_modln_input(bf, x, L, D, mod + 0 * D, mod + 1 * D, cfg->ln_eps, ws.a, st);
+  if (e != hipSuccess) return device_status(e);
+  if (bf) {
+    typedef const bf16_t* P;
+    GemmBf16Args g{};
+    // q = a[idx] Wq^T + bq
+    g = GemmBf16Args{static_cast<P>(ws.a), D, idx, static_cast<P>(w->wq), static_cast<P>(w->wq), D, D,
+                     static_cast<P>(w->bq), static_cast<P>(w->bq), n, D, D, ws.q, D,
+                     nullptr, nullptr, 0, nullptr, 0};
+    if ((e = launch_gemm_bf16("gemm_q_bf16", 0, g, st)) != hipSuccess) return device_status(e);
+    // [k | v] = a [Wk; Wv]^T + [bk; bv], one N = 2D GEMM over all L rows
+    g = GemmBf16Args{static_cast<P>(ws.a), D, nullptr, static_cast<P>(w->wk), static_cast<P>(w->wv), D,
+                     D, static_cast<P>(w->bk), static_cast<P>(w->bv), L, 2 * D, D, ws.kv, 2 * D,
+                     nullptr, nullptr, 0, nullptr, 0};
+    if ((e = launch_gemm_bf16("gemm_kv_bf16", 0, g, st)) != hipSuccess) return device_status(e);
+    const bf16_t* kvp = static_cast<const bf16_t*>(ws.kv);
+    if ((e = launch_attn_bf16(static_cast<P>(ws.q), D, kvp, kvp + D, 2 * D, n, L, H,
+                              static_cast<bf16_t*>(ws.o), D, st)) != hipSuccess)
+      return device_status(e);
+    // x1 = x[idx] + gate1 * (o Wo^T + bo)
+    g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, static_cast<P>(w->wo), static_cast<P>(w->wo), D,
+                     D, static_cast<P>(w->bo), static_cast<P>(w->bo), n, D, D, ws.x1, D,
+                     mod + 2 * D, x, D, idx, 1};
+    if ((e = launch_gemm_bf16("gemm_o_bf16", 2, g, st)) != hipSuccess) return device_status(e);
+    if ((e = launch_modln_x1(1, ws.x1, n, D, mod + 3 * D, mod + 4 * D, cfg->ln_eps, ws.b, st)) !=
+        hipSuccess)
+      return device_status(e);
+    // h = GELU(b W1^T + b1)
+    g = GemmBf16Args{static_cast<P>(ws.b), D, nullptr, static_cast<P>(w->w1), static_cast<P>(w->w1), F,
+                     D, static_cast<P>(w->b1), static_cast<P>(w->b1), n, F, D, ws.h, F,
+                     nullptr, nullptr, 0, nullptr, 0};
+    if ((e = launch_gemm_bf16("gemm_ffn_up_bf16", 1, g, st)) != hipSuccess) return device_status(e);
+    // y_sel = x1 + gate2 * (h W2^T + b2)
+    g = GemmBf16Args{static_cast<P>(ws.h), F, nullptr, static_cast<P>(w->w2), static_cast<P>(w->w2), D,
+                     F, static_cast<P>(w->b2), static_cast<P>(w->b2), n, D, F, y_sel, D,
+                     mod + 5 * D, ws.x1, D, nullptr, 0};
+    if ((e = launch_gemm_bf16("gemm_ffn_down_bf16", 2, g, st)) != hipSuccess) return device_status(e);
+    return ECHO_OK;
+  }
+  typedef const float* P;
+  const int dh = D / H;
+  GemmF32Args g{};
+  g = GemmF32Args{static_cast<P>(ws.a), D, idx, static_cast<P>(w->wq), static_cast<P>(w->wq), D, D,
+                  static_cast<P>(w->bq), static_cast<P>(w->bq), n, D, D, static_cast<float*>(ws.q), D,
+                  nullptr, nullptr, 0, nullptr};
+  if ((e = launch_gemm_f32("gemm_q_f32", 0, g, st)) != hipSuccess) return device_status(e);
+  g = GemmF32Args{static_cast<P>(ws.a), D, nullptr, static_cast<P>(w->wk), static_cast<P>(w->wv), D, D,
+                  static_cast<P>(w->bk), static_cast<P>(w->bv), L, 2 * D, D,
+                  static_cast<float*>(ws.kv), 2 * D, nullptr, nullptr, 0, nullptr};
+  if ((e = launch_gemm_f32("gemm_kv_f32", 0, g, st)) != hipSuccess) return device_status(e);
+  const float* kvp = static_cast<const float*>(ws.kv);
+  if ((e = launch_attn_f32(static_cast<P>(ws.q), D, kvp, kvp + D, 2 * D, n, L, H, dh,
+                           static_cast<float*>(ws.o), D, st)) != hipSuccess)
+    return device_status(e);
+  g = GemmF32Args{static_cast<P>(ws.o), D, nullptr, static_cast<P>(w->wo), static_cast<P>(w->wo), D, D,
+                  static_cast<P>(w->bo), static_cast<P>(w->bo), n, D, D, ws.x1, D, mod + 2 * D,
+                  static_cast<P>(x), D, idx};
+  if ((e = launch_gemm_f32("gemm_o_f32", 2, g, st)) != hipSuccess) return device_status(e);
+  if ((e = launch_modln_x1(0, ws.x1, n, D, mod + 3 * D, mod + 4 * D, cfg->ln_eps, ws.b, st)) !=
+      hipSuccess)
+    return device_status(e);
+  g = GemmF32Args{static_cast<P>(ws.b), D, nullptr, static_cast<P>(w->w1), static_cast<P>(w->w1), F, D,
+                  static_cast<P>(w->b1), static_cast<P>(w->b1), n, F, D, static_cast<float*>(ws.h), F,
+                  nullptr, nullptr, 0, nullptr};
+  if ((e = launch_gemm_f32("gemm_ffn_up_f32", 1, g, st)) != hipSuccess) return device_status(e);
+  g = GemmF32Args{static_cast<P>(ws.h), F, nullptr, static_cast<P>(w->w2), static_cast<P>(w->w2), D, F,
+                  static_cast<P>(w->b2), static_cast<P>(w->b2), n, D, F, y_sel, D, mod + 5 * D, ws.x1,
+                  D, nullptr};
+  if ((e = launch_gemm_f32("gemm_ffn_down_f32", 2, g, st)) != hipSuccess) return device_status(e);
+  return ECHO_OK;
+}
+
+int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* idx, const uint8_t* mask,
+                      int32_t n_sel, const float* y_sel, void* xref, int8_t* codes, float* scale,
+                      void* y, void* stream) {
+  if (cfg == nullptr || cfg->L < 1 || cfg->D < 8 || (cfg->D % 8) != 0 || cfg->D > 16384 ||
+      !ok_dtype(cfg->dtype))
+    return ECHO_EINVAL;
+  if (n_sel < 0 || n_sel > cfg->L) return ECHO_EINVAL;
+  if (!ok_ptr(x) || !ok_ptr(mask) || !ok_ptr(xref) || !ok_ptr(codes) || !ok_ptr(scale) || !ok_ptr(y))
+    return ECHO_EINVAL;
+  if (n_sel > 0 && (!ok_ptr(idx) || !ok_ptr(y_sel))) return ECHO_EINVAL;
+  return device_status(launch_cache_update(cfg->dtype == ECHO_BF16, x, idx, mask, n_sel, cfg->L, cfg->D,
+                                           y_sel, xref, codes, scale, y,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int echo_profile_enable(int on) {
+  profile_set(on != 0);
+  return ECHO_OK;
+}
+
+int echo_profile_read(echo_kernel_time* out, int32_t max) {
+  if (max < 0 || (max > 0 && out == nullptr)) return -ECHO_EINVAL;
+  int n = 0;
+  int status = ECHO_OK;
+  for (const TimingRecord& r : g_records) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) {
+      g_last_hip_error = static_cast<int>(e);
+      status = ECHO_EDEVICE;
+    }
+    int slot = -1;
+    for (int i = 0; i < n; ++i)
+      if (strcmp(out[i].name, r.name) == 0) slot = i;
+    if (slot < 0 && n < max) {
+      slot = n++;
+      out[slot].name = r.name;
+      out[slot].launches = 0;
+      out[slot].total_ms = 0.0;
+    }
+    if (slot >= 0) {
+      out[slot].launches += 1;
+      out[slot].total_ms += ms;
+    }
+    g_event_pool.push_back(r.start);
+    g_event_pool.push_back(r.stop);
+  }
+  g_records.clear();
+  return status == ECHO_OK ? n : -status;
+}
+
+}  // extern "C"

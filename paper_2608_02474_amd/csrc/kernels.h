@@ -1,0 +1,82 @@
+// Launchers of the gfx950 kernels, shared by the kernel files and the C ABI.
+// Every launcher enqueues on `stream` and returns the launch error.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace echo {
+
+typedef uint16_t bf16_t;
+
+enum GemmEpi { EPI_BIAS = 0, EPI_GELU = 1, EPI_GATE_RES = 2 };
+
+// C[m, n] = epilogue(sum_k A[row(m), k] B[n, k] + bias[n]), see gemm_bf16.hip.
+struct GemmBf16Args {
+  const bf16_t* A;
+  int64_t lda;
+  const int32_t* a_rows;    // optional: A row of output row m is a_rows[m]
+  const bf16_t* B0;
+  const bf16_t* B1;         // rows n >= n_split come from B1 (row n - n_split)
+  int n_split;
+  int64_t ldb;
+  const bf16_t* bias0;
+  const bf16_t* bias1;
+  int M, N, K;
+  void* C;                  // bf16 (EPI_BIAS, EPI_GELU) or fp32 (EPI_GATE_RES)
+  int64_t ldc;
+  const float* gate;        // [N], EPI_GATE_RES
+  const void* res;          // EPI_GATE_RES residual rows (bf16 or fp32)
+  int64_t ldr;
+  const int32_t* res_rows;  // optional gather of residual rows
+  int res_bf16;
+};
+
+struct GemmF32Args {
+  const float* A;
+  int64_t lda;
+  const int32_t* a_rows;
+  const float* B0;
+  const float* B1;
+  int n_split;
+  int64_t ldb;
+  const float* bias0;
+  const float* bias1;
+  int M, N, K;
+  float* C;
+  int64_t ldc;
+  const float* gate;
+  const float* res;
+  int64_t ldr;
+  const int32_t* res_rows;
+};
+
+hipError_t launch_energy(const float* audio, int64_t n_samples, int T, int sr, int n_fft, int hop,
+                         int n_bands, float* band_energy, float* frame_energy, float* frame_weight,
+                         double* part, double* e_scratch, hipStream_t stream);
+int energy_max_frames(int64_t n_samples, int T, int n_fft, int hop);
+
+hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
+                         int D, double xi, int k, int threshold_mode, float threshold, float* s,
+                         double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
+                         double* step_delta, hipStream_t stream);
+
+hipError_t launch_cache_update(int dtype_bf16, const void* x, const int32_t* idx, const uint8_t* mask,
+                               int n_sel, int L, int D, const float* y_sel, void* xref, int8_t* codes,
+                               float* scale, void* y, hipStream_t stream);
+
+hipError_t launch_modln_input(int dtype_bf16, const void* x, int M, int D, const float* shift,
+                              const float* scale, float eps, void* out, hipStream_t stream);
+hipError_t launch_modln_x1(int dtype_bf16, const float* x1, int M, int D, const float* shift,
+                           const float* scale, float eps, void* out, hipStream_t stream);
+
+hipError_t launch_gemm_bf16(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream);
+hipError_t launch_gemm_f32(const char* name, int epi, const GemmF32Args& a, hipStream_t stream);
+
+hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
+                            int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
+                            hipStream_t stream);
+hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, const float* v, int64_t ldkv,
+                           int Mq, int L, int H, int dh, float* out, int64_t ldo, hipStream_t stream);
+
+}  // namespace echo

@@ -1,0 +1,234 @@
+// Saliency and recompute selection (Sec. 3.1 Eq. 1, applied per token against
+// its cached input; Sec. 3.3 saliency mask with k = ceil(r L) tokens).
+//
+// saliency_rows: one wave per token row streams x and xref with 16-byte loads
+//   and accumulates |x - xref| and |xref| in fp64 (exact per-element
+//   differences, so only the summation order differs from the definition).
+//   Writes s_i = fp32(w_frame * num / (den + xi)) plus num/den for the step sum.
+// select_rows: one 1024-thread workgroup
+//   (1) step-level Eq. 1 sum in a fixed order (deterministic);
+//   (2) top-K threshold key by 4-pass 8-bit radix select over order-preserving
+//       uint32 keys (histograms in LDS);
+//   (3) stable compaction in index order: wave ballot + popcount gives each
+//       lane's rank among equal-key tokens and its output slot; ties at the
+//       threshold key go to the lowest indices.
+// The key set is tiny (4 bytes per token, L2-resident), so one workgroup keeps
+// the selection exact and deterministic at a cost of a few microseconds.
+#include "common.h"
+#include "kernels.h"
+#include "launch.h"
+
+namespace echo {
+
+constexpr int kSalThreads = 256;
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / kWave;
+
+template <typename T>
+__global__ void __launch_bounds__(kSalThreads)
+saliency_rows(const T* __restrict__ x, const T* __restrict__ xref, const float* __restrict__ fw,
+              int L, int N, int D, double xi, float* __restrict__ s_out,
+              double* __restrict__ num_out, double* __restrict__ den_out) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * (kSalThreads / kWave) + wave;
+  if (row >= L) return;
+  constexpr int V = Elem<T>::kPerVec;
+  const T* xr = x + row * D;
+  const T* rr = xref + row * D;
+  const int nvec = D / V;
+  double num = 0.0, den = 0.0;
+#pragma unroll 4
+  for (int c = lane; c < nvec; c += kWave) {
+    const uint4 a = ldg16(xr + static_cast<int64_t>(c) * V);
+    const uint4 b = ldg16(rr + static_cast<int64_t>(c) * V);
+    float fa[V], fb[V];
+    unpack16(a, fa, static_cast<const T*>(nullptr));
+    unpack16(b, fb, static_cast<const T*>(nullptr));
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const double da = fa[j], db = fb[j];
+      num += fabs(da - db);
+      den += fabs(db);
+    }
+  }
+  num = wave_sum(num);
+  den = wave_sum(den);
+  if (lane == 0) {
+    const double delta = num / (den + xi);
+    const double w = static_cast<double>(fw[row / N]);
+    s_out[row] = __double2float_rn(w * delta);
+    num_out[row] = num;
+    den_out[row] = den;
+  }
+}
+
+// Order-preserving key: larger float -> larger key; NaN above everything; -0 == +0.
+__device__ __forceinline__ uint32_t rank_key(float s) {
+  if (s != s) return 0xffffffffu;
+  uint32_t u = __float_as_uint(s);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__global__ void __launch_bounds__(kSelThreads)
+select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float threshold,
+            const double* __restrict__ num, const double* __restrict__ den, double xi,
+            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel,
+            double* __restrict__ step_delta) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t sh_digit, sh_above;
+  __shared__ uint32_t wcnt[2][kSelWaves];
+  __shared__ double red_n[kSelWaves], red_d[kSelWaves];
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+
+  // (1) step-level relative change, fixed summation order
+  if (step_delta != nullptr) {
+    double a = 0.0, b = 0.0;
+    for (int i = tid; i < L; i += kSelThreads) {
+      a += num[i];
+      b += den[i];
+    }
+    a = wave_sum(a);
+    b = wave_sum(b);
+    if (lane == 0) {
+      red_n[wave] = a;
+      red_d[wave] = b;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      double sa = 0.0, sb = 0.0;
+      for (int w = 0; w < kSelWaves; ++w) {
+        sa += red_n[w];
+        sb += red_d[w];
+      }
+      *step_delta = sa / (sb + xi);
+    }
+  }
+
+  // (2) threshold key and how many tokens equal to it are taken
+  uint32_t thr;
+  uint32_t need_eq;
+  bool take_eq;
+  if (threshold_mode) {
+    thr = rank_key(threshold);
+    need_eq = 0;
+    take_eq = false;
+  } else if (k == 0) {
+    thr = 0xffffffffu;
+    need_eq = 0;
+    take_eq = true;
+  } else {
+    uint32_t prefix = 0, pmask = 0, kk = static_cast<uint32_t>(k);
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+      for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
+      __syncthreads();
+      for (int i = tid; i < L; i += kSelThreads) {
+        const uint32_t key = rank_key(s[i]);
+        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 0xffu], 1u);
+      }
+      __syncthreads();
+      if (wave == 0) {
+        // lane covers bins 255-4*lane down to 252-4*lane; lane 0 holds the top bins
+        uint32_t c[4];
+        uint32_t tot = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          c[j] = hist[255 - 4 * lane - j];
+          tot += c[j];
+        }
+        uint32_t incl = tot;  // inclusive scan from lane 0
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint32_t v = __shfl_up(incl, o);
+          if (lane >= o) incl += v;
+        }
+        const uint64_t hit = __ballot(incl >= kk);
+        const int first = __ffsll(static_cast<long long>(hit)) - 1;  // kk <= matching count
+        if (lane == first) {
+          uint32_t above = incl - tot;
+          int digit = 255 - 4 * lane;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (above + c[j] >= kk) {
+              digit = 255 - 4 * lane - j;
+              break;
+            }
+            above += c[j];
+          }
+          sh_digit = static_cast<uint32_t>(digit);
+          sh_above = above;
+        }
+      }
+      __syncthreads();
+      prefix |= sh_digit << shift;
+      pmask |= 0xffu << shift;
+      kk -= sh_above;
+      __syncthreads();  // hist and sh_* are rewritten by the next pass
+    }
+    thr = prefix;
+    need_eq = kk;
+    take_eq = true;
+  }
+
+  // (3) stable compaction in index order
+  uint32_t base_eq = 0, base_sel = 0;
+  for (int c0 = 0; c0 < L; c0 += kSelThreads) {
+    const int i = c0 + tid;
+    const bool valid = i < L;
+    const uint32_t key = valid ? rank_key(s[i]) : 0u;
+    const bool gt = valid && key > thr;
+    const bool eq = valid && take_eq && key == thr;
+    const uint64_t beq = __ballot(eq);
+    if (lane == 0) wcnt[0][wave] = static_cast<uint32_t>(__popcll(beq));
+    __syncthreads();
+    uint32_t eq_before = base_eq, eq_total = 0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      const uint32_t v = wcnt[0][w];
+      if (w < wave) eq_before += v;
+      eq_total += v;
+    }
+    eq_before += static_cast<uint32_t>(__popcll(beq & lt_mask));
+    const bool sel = gt || (eq && eq_before < need_eq);
+    const uint64_t bsel = __ballot(sel);
+    if (lane == 0) wcnt[1][wave] = static_cast<uint32_t>(__popcll(bsel));
+    __syncthreads();
+    uint32_t pos = base_sel, sel_total = 0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      const uint32_t v = wcnt[1][w];
+      if (w < wave) pos += v;
+      sel_total += v;
+    }
+    pos += static_cast<uint32_t>(__popcll(bsel & lt_mask));
+    if (valid) {
+      mask[i] = sel ? 1 : 0;
+      if (sel) idx[pos] = i;
+    }
+    base_eq += eq_total;
+    base_sel += sel_total;
+    __syncthreads();  // wcnt is rewritten by the next chunk
+  }
+  if (tid == 0) *n_sel = static_cast<int32_t>(base_sel);
+}
+
+hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
+                         int D, double xi, int k, int threshold_mode, float threshold, float* s,
+                         double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
+                         double* step_delta, hipStream_t stream) {
+  const dim3 grid((L + (kSalThreads / kWave) - 1) / (kSalThreads / kWave));
+  hipError_t e;
+  if (dtype_bf16)
+    e = ECHO_LAUNCH("saliency_rows_bf16", saliency_rows<bf16_t>, grid, dim3(kSalThreads), 0, stream,
+                    static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(xref), fw, L, N, D, xi,
+                    s, num, den);
+  else
+    e = ECHO_LAUNCH("saliency_rows_f32", saliency_rows<float>, grid, dim3(kSalThreads), 0, stream,
+                    static_cast<const float*>(x), static_cast<const float*>(xref), fw, L, N, D, xi,
+                    s, num, den);
+  if (e != hipSuccess) return e;
+  return ECHO_LAUNCH("select_rows", select_rows, dim3(1), dim3(kSelThreads), 0, stream, s, L, k,
+                     threshold_mode, threshold, num, den, xi, idx, mask, n_sel, step_delta);
+}
+
+}  // namespace echo

@@ -1,0 +1,55 @@
+"""Algorithmic work of each kernel of the cached block step, and MI355X peaks.
+
+Algorithmic = what the method must compute or move, not what a kernel happens
+to re-read: FLOPs for the contractions, HBM bytes for the streaming kernels.
+Symbols: L tokens, K recomputed tokens, U = L - K, D hidden, F FFN width,
+b activation bytes (2 for bf16, 4 for fp32).
+"""
+from __future__ import annotations
+
+# MI355X published peaks.  bf16 dense MFMA = 256 CU x 2.4 GHz x 4096 flop/clk.
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def kernel_work(L: int, K: int, D: int, F: int, b: int, n_samples: int = 0):
+    """{kernel name prefix: (amount per launch, "flop" | "byte")}.
+
+    The names are the ones the library records for each launch; GEMMs are
+    named after their call site (q, kv, o, ffn_up, ffn_down).
+    """
+    U = L - K
+    return {
+        # saliency: read x and xref, write s, num, den
+        "saliency_rows": (2 * L * D * b + 20 * L, "byte"),
+        # selection: a few passes over 4-byte keys (latency-bound); write idx, mask
+        "select_rows": (4 * L + 4 * K + L, "byte"),
+        # LN1 over all rows: read x, write a
+        "modln_in": (2 * L * D * b, "byte"),
+        "gemm_q": (2 * K * D * D, "flop"),
+        "gemm_kv": (4 * L * D * D, "flop"),
+        "attn_fwd": (4 * K * L * D, "flop"),
+        "gemm_o": (2 * K * D * D, "flop"),
+        # LN2 over the recomputed rows: read x1 (fp32), write b
+        "modln_x1": (K * D * (4 + b), "byte"),
+        "gemm_ffn_up": (2 * K * D * F, "flop"),
+        "gemm_ffn_down": (2 * K * F * D, "flop"),
+        # cache update: fresh rows read y_sel (fp32) and x, write xref, codes, y;
+        # reused rows read xref and codes and write y; plus scale and mask
+        "cache_update": (K * D * (4 + b + b + 1 + b) + U * D * (b + 1 + b) + 4 * L + L, "byte"),
+        # energy: read the audio once (latency-bound, once per clip)
+        "energy_frames": (4 * n_samples, "byte"),
+        "energy_reduce": (0, "byte"),
+    }
+
+
+def work_of(name: str, table: dict):
+    for prefix, v in table.items():
+        if name.startswith(prefix):
+            return v
+    return None
+
+
+def block_flops(L: int, K: int, D: int, F: int) -> int:
+    return 2 * K * D * D + 4 * L * D * D + 4 * K * L * D + 2 * K * D * D + 4 * K * D * F

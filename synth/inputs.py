@@ -5,10 +5,16 @@ holds no arithmetic of the method itself: it draws audio, latents, weights and
 modulation vectors, and rounds inputs to the storage precision (bf16, round to
 nearest even) so that both sides see identical values.
 
-Every draw uses ``np.random.default_rng([seed, stream])`` with a fixed stream
-number per tensor family, so any tensor can be regenerated on its own.
+Every draw uses ``np.random.default_rng([seed, stream, ...])`` with a fixed
+stream number per tensor family, so any tensor can be regenerated on its own.
+Large matrices are drawn in fixed blocks of rows, each block from its own
+generator ``[seed, stream, sub, block]``, so the values do not depend on how
+many threads fill them.
 """
 from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -19,6 +25,32 @@ STREAM_WEIGHTS, STREAM_BIAS, STREAM_MOD, STREAM_XREF, STREAM_DRIFT, STREAM_AUDIO
 
 def _rng(seed: int, stream: int, sub: int = 0) -> np.random.Generator:
     return np.random.default_rng([seed, stream, sub])
+
+
+_BLOCK_ROWS = 1024
+_THREADS = min(16, os.cpu_count() or 1)
+
+
+def _normal_rows(seed: int, stream: int, sub: int, shape, scale: float = 1.0,
+                 dtype: str | None = None) -> np.ndarray:
+    """scale * N(0, 1) of `shape` (rows x cols), optionally storage-rounded,
+    drawn in blocks of _BLOCK_ROWS rows (block b from [seed, stream, sub, b])."""
+    rows = shape[0]
+    cols = int(np.prod(shape[1:])) if len(shape) > 1 else 1
+    out = np.empty((rows, cols), dtype=np.float32)
+
+    def fill(b):
+        r0, r1 = b * _BLOCK_ROWS, min(rows, (b + 1) * _BLOCK_ROWS)
+        g = np.random.default_rng([seed, stream, sub, b])
+        blk = g.standard_normal((r1 - r0, cols), dtype=np.float32)
+        if scale != 1.0:
+            blk *= np.float32(scale)
+        out[r0:r1] = storage_round(blk, dtype) if dtype else blk
+
+    nb = -(-rows // _BLOCK_ROWS)
+    with ThreadPoolExecutor(_THREADS) as ex:
+        list(ex.map(fill, range(nb)))
+    return out.reshape(shape)
 
 
 # ---------------------------------------------------------------- bf16 storage
@@ -137,13 +169,19 @@ def make_latents(w: Workload, seed: int | None = None):
     per latent frame, so frames drift by different amounts.
     """
     seed = w.seed if seed is None else seed
-    rx = _rng(seed, STREAM_XREF)
-    xref = rx.standard_normal((w.L, w.D), dtype=np.float32)
-    rd = _rng(seed, STREAM_DRIFT)
-    sigma = rd.uniform(0.01, 0.3, size=w.T).astype(np.float32)
-    noise = rd.standard_normal((w.L, w.D), dtype=np.float32)
-    x = xref + np.repeat(sigma, w.N)[:, None] * noise
-    return storage_round(xref, w.dtype), storage_round(x, w.dtype)
+    xref = _normal_rows(seed, STREAM_XREF, 0, (w.L, w.D))
+    sigma = _rng(seed, STREAM_DRIFT).uniform(0.01, 0.3, size=w.T).astype(np.float32)
+    x = _normal_rows(seed, STREAM_DRIFT, 1, (w.L, w.D))
+    row_sigma = np.repeat(sigma, w.N)[:, None]
+
+    def mix(b):
+        r0, r1 = b * _BLOCK_ROWS, min(w.L, (b + 1) * _BLOCK_ROWS)
+        x[r0:r1] = storage_round(xref[r0:r1] + row_sigma[r0:r1] * x[r0:r1], w.dtype)
+        xref[r0:r1] = storage_round(xref[r0:r1], w.dtype)
+
+    with ThreadPoolExecutor(_THREADS) as ex:
+        list(ex.map(mix, range(-(-w.L // _BLOCK_ROWS))))
+    return xref, x
 
 
 def make_block_weights(w: Workload, seed: int | None = None, gate_mean=None,
@@ -164,8 +202,7 @@ def make_block_weights(w: Workload, seed: int | None = None, gate_mean=None,
               "w1": (F, D), "w2": (D, F)}
     out = {}
     for i, (k, shp) in enumerate(shapes.items()):
-        r = _rng(seed, STREAM_WEIGHTS, i)
-        out[k] = storage_round(0.02 * r.standard_normal(shp, dtype=np.float32), w.dtype)
+        out[k] = _normal_rows(seed, STREAM_WEIGHTS, i, shp, scale=0.02, dtype=w.dtype)
     bshapes = {"bq": D, "bk": D, "bv": D, "bo": D, "b1": F, "b2": D}
     for i, (k, n) in enumerate(bshapes.items()):
         r = _rng(seed, STREAM_BIAS, i)

@@ -1,0 +1,313 @@
+"""GPU parity: every C-ABI call against the CPU oracle on the same seeded
+inputs, at sizes the oracle finishes in seconds (element by element) and at
+the full 32760- and 75600-token block shapes (sampled rows the oracle computes
+one by one, plus properties that hold at any size)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import block as OB
+from oracle import cache as OC
+from oracle import energy as OE
+from oracle import select as OS
+from oracle import step as OST
+from paper_2608_02474_amd import api
+
+from gpu_util import (check_block, check_selection, device, down, params_to_device, say, tdtype,
+                      up, TOL_BF16_ABS, TOL_F32_ABS)
+
+pytestmark = pytest.mark.gpu
+
+# a small bf16 shape that is ragged against every tile size (GEMM 256, attention 128/64)
+RAGGED = synth.Workload("ragged_bf16_300tok", T=3, grid=(10, 10), D=256, H=2, F=512,
+                        n_samples=4000, ratio=0.37, dtype="bf16", audio="bursts", seed=21)
+RAGGED_F32 = RAGGED.with_(name="ragged_f32_300tok", dtype="f32", H=4, seed=22)
+
+
+def _bits(a):
+    a = np.ascontiguousarray(a)
+    return a.view(np.uint32) if a.dtype == np.float32 else a
+
+
+# ------------------------------------------------------------------- energy
+
+@pytest.mark.parametrize("profile,n,T", [
+    ("bursts", 8000, 2), ("bursts", 20000, 5), ("speech", 81000, 21), ("noise", 81000, 21),
+    ("half_silence", 81000, 21), ("speech", 1000, 3), ("speech", 4000, 1)])
+def test_energy_matches_oracle(profile, n, T):
+    say(f"energy {profile} n={n} T={T}")
+    audio = synth.make_audio(profile, n, 16000, seed=11)
+    Eb, e, w = OE.energy(audio, T)
+    gb, ge, gw = api.energy(up(audio), T)
+    torch.cuda.synchronize()
+    gb, ge, gw = down(gb), down(ge), down(gw)
+    for got, want, name in ((gb, Eb, "band"), (ge, e, "frame"), (gw, w, "weight")):
+        err = np.abs(got.astype(np.float64) - want)
+        assert (err <= 1e-6 * np.abs(want.astype(np.float64))).all(), (name, float(err.max()))
+    if profile == "half_silence":
+        assert (ge[: T // 2] == 0).all()
+
+
+# ------------------------------------------------------------------- select
+
+def _frame_weight(w, profile=None):
+    audio = synth.make_audio(profile or w.audio, w.n_samples, 16000, w.seed)
+    return OE.energy(audio, w.T)[2]
+
+
+def _select_case(w, ks, fw=None, profile=None):
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w, profile) if fw is None else fw
+    s, num, den = OS.saliency(x, xref, fw, w.N)
+    dt = tdtype(w.dtype)
+    X, XR, FW = up(x, dt), up(xref, dt), up(fw)
+    for K in ks:
+        say(f"select {w.name} profile={profile or w.audio} K={K}")
+        sel = api.select(X, XR, FW, w.N, k=K)
+        torch.cuda.synchronize()
+        gs = down(sel.saliency)
+        assert (np.abs(gs.astype(np.float64) - s) <= 1e-6 * np.abs(s.astype(np.float64))).all()
+        gi = down(sel.idx)[:K]
+        nd = check_selection(gi, OS.select_topk(s, K), s, K) if K else 0
+        if K == 0:
+            assert len(gi) == 0
+        m = down(sel.mask)
+        assert m.sum() == K and (m[gi] == 1).all()
+        assert int(down(sel.n_sel_dev)[0]) == K
+        sd = float(down(sel.step_delta)[0])
+        assert sd == pytest.approx(OS.step_delta(num, den), rel=1e-12)
+        say(f"  ok ({nd} tie-excluded differences)")
+    return s, X, XR, FW
+
+
+def test_select_tiny_f32():
+    w = synth.TINY
+    _select_case(w, [0, 1, w.K, w.L - 1, w.L])
+
+
+def test_select_ragged_with_ties():
+    # frame weights with zeros: exact zero-saliency ties resolved by index
+    w = RAGGED_F32
+    fw = np.array([0.0, 0.6, 0.0], np.float32)
+    _select_case(w, [0, 1, 99, 100, 101, 150, 299, 300], fw=fw)
+
+
+def test_select_small_bf16():
+    w = synth.SMALL
+    _select_case(w, [w.K, 1, w.L])
+
+
+def test_select_threshold_mode():
+    w = synth.SMALL
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w)
+    s, _, _ = OS.saliency(x, xref, fw, w.N)
+    dt = tdtype(w.dtype)
+    for th in (float(np.median(s)), float(np.quantile(s, 0.9)), 0.0, 1e9):
+        sel = api.select(up(x, dt), up(xref, dt), up(fw), w.N, threshold=th)
+        torch.cuda.synchronize()
+        n = sel.count()
+        want = OS.select_threshold(s, th)
+        got = down(sel.idx)[:n]
+        # identical saliencies (checked above to 1e-6) decide identically except at the threshold
+        diff = set(got.tolist()) ^ set(want.tolist())
+        for i in diff:
+            assert abs(float(s[i]) - th) <= 1e-6 * max(abs(th), 1e-30)
+        assert list(got) == sorted(got)
+
+
+@pytest.mark.parametrize("profile", synth.SWEEP_AUDIO)
+def test_select_14b_shape_sweep(profile):
+    w = synth.WAN14B_480P.with_(audio=profile, seed=3)
+    ks = [synth.WAN14B_480P.with_(ratio=r).K for r in synth.SWEEP_RATIOS] + [w.K]
+    _select_case(w, ks)
+
+
+def test_select_720p_shape():
+    w = synth.WAN14B_720P
+    _select_case(w, [w.K])
+
+
+# -------------------------------------------------------------------- cache
+
+@pytest.mark.parametrize("w", [synth.TINY, RAGGED, synth.SMALL, synth.WAN14B_480P],
+                         ids=lambda w: w.name)
+def test_cache_update_bit_exact(w):
+    say(f"cache {w.name}")
+    xref, x = synth.make_latents(w)
+    rng = np.random.default_rng(5)
+    L, D, K = w.L, w.D, w.K
+    idx = np.sort(rng.choice(L, K, replace=False)).astype(np.int32)
+    y_sel = (x[idx] + 0.1 * rng.standard_normal((K, D))).astype(np.float32)
+    y_sel[0] = x[idx[0]]                                   # zero residual -> scale 0, codes 0
+    y_sel[-1] = x[idx[-1]]
+    y_sel[-1, 7] += 3.0                                    # one-hot residual -> +127
+    codes0 = rng.integers(-127, 128, (L, D)).astype(np.int8)
+    scale0 = rng.uniform(0, 0.02, L).astype(np.float32)
+    y_o, xr_o, c_o, s_o = OC.cache_update(x, idx, y_sel, xref, codes0, scale0, w.dtype)
+    dt = tdtype(w.dtype)
+    XR, C, S = up(xref, dt), up(codes0), up(scale0)
+    mask = OS.mask_of(idx, L)
+    Y = api.cache_update(up(x, dt), up(idx), up(mask), K, up(y_sel), XR, C, S)
+    torch.cuda.synchronize()
+    assert np.array_equal(down(C), c_o)
+    assert np.array_equal(_bits(down(S)), _bits(s_o))
+    assert np.array_equal(_bits(down(XR)), _bits(xr_o))
+    assert np.array_equal(_bits(down(Y)), _bits(y_o))
+    assert down(S)[idx[0]] == 0 and (down(C)[idx[0]] == 0).all()
+    assert down(C)[idx[-1], 7] == 127
+
+
+def test_cache_update_empty_and_full():
+    w = synth.SMALL
+    xref, x = synth.make_latents(w)
+    rng = np.random.default_rng(6)
+    codes0 = rng.integers(-127, 128, (w.L, w.D)).astype(np.int8)
+    scale0 = rng.uniform(0, 0.02, w.L).astype(np.float32)
+    dt = tdtype(w.dtype)
+    # K = 0: output is the dequantized cache everywhere
+    y_o, _, _, _ = OC.cache_update(x, np.zeros(0, np.int64), np.zeros((0, w.D), np.float32), xref,
+                                   codes0, scale0, w.dtype)
+    Y = api.cache_update(up(x, dt), None, up(np.zeros(w.L, np.uint8)), 0, None, up(xref, dt),
+                         up(codes0), up(scale0))
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(down(Y)), _bits(y_o))
+    # K = L: every row fresh
+    idx = np.arange(w.L, dtype=np.int32)
+    y_sel = (x + 0.05 * rng.standard_normal(x.shape)).astype(np.float32)
+    y_o, xr_o, c_o, s_o = OC.cache_update(x, idx, y_sel, xref, codes0, scale0, w.dtype)
+    C = up(codes0)
+    Y = api.cache_update(up(x, dt), up(idx), up(np.ones(w.L, np.uint8)), w.L, up(y_sel),
+                         up(xref, dt), C, up(scale0))
+    torch.cuda.synchronize()
+    assert np.array_equal(down(C), c_o)
+    assert np.array_equal(_bits(down(Y)), _bits(y_o))
+
+
+# -------------------------------------------------------------------- block
+
+def _block_gpu(w, p, x, idx):
+    P = params_to_device(p, w.dtype)
+    ys = api.block_partial(P, up(x, tdtype(w.dtype)), up(np.asarray(idx, np.int32)), len(idx), w.H)
+    torch.cuda.synchronize()
+    return down(ys)
+
+
+@pytest.mark.parametrize("w", [synth.TINY, RAGGED_F32, RAGGED, synth.SMALL], ids=lambda w: w.name)
+def test_block_partial_full_compare(w):
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    rng = np.random.default_rng(7)
+    cases = {"topK": np.sort(rng.choice(w.L, w.K, replace=False)),
+             "one": np.array([w.L - 1]), "all": np.arange(w.L)}
+    if w.L <= 300:
+        cases["unsorted_repeats"] = np.array([5, 3, 3, w.L - 1, 0])
+    kv = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    for name, idx in cases.items():
+        say(f"block {w.name} {name} n={len(idx)}")
+        got = _block_gpu(w, p, x, idx)
+        want = OB.block_partial(p, x, idx, w.H, kv=kv)
+        check_block(got, want, w.dtype, f"{w.name}/{name}")
+
+
+def test_block_gates_one_informational():
+    # gates ~ N(1, 0.1): larger bf16 error budget; reported, bounded loosely
+    w = RAGGED
+    p = synth.make_block_weights(w, gate_mean=1.0, gate_std=0.1)
+    _, x = synth.make_latents(w)
+    idx = np.arange(w.L)
+    got = _block_gpu(w, p, x, idx)
+    want = OB.block_partial(p, x, idx, w.H)
+    err = np.abs(got - want)
+    say(f"  gates~N(1,0.1): max|err| {err.max():.3e}")
+    assert err.max() < 0.1
+
+
+@pytest.mark.parametrize("w", [synth.WAN14B_480P, synth.WAN14B_720P], ids=lambda w: w.name)
+def test_block_partial_full_size_sampled(w):
+    """Full-size block in the launch configuration the benchmark times; the
+    oracle computes the all-row K/V projection and then sampled rows."""
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w)
+    s, _, _ = OS.saliency(x, xref, fw, w.N)
+    idx = OS.select_topk(s, w.K)
+    say(f"block {w.name} K={w.K} (GPU)")
+    got = _block_gpu(w, p, x, idx)
+    rng = np.random.default_rng(8)
+    rows = np.unique(np.concatenate([[0, w.K - 1, w.K // 2],
+                                     rng.choice(w.K, 29, replace=False)]))
+    say(f"block {w.name}: oracle on {len(rows)} sampled rows")
+    want = OB.block_partial(p, x, idx[rows], w.H)
+    check_block(got[rows], want, w.dtype, f"{w.name}/sampled")
+
+
+def test_block_row_independence_full_size():
+    """Any selection gives exactly the rows of the all-token block (GPU vs GPU,
+    bit-exact): holds at any size, checked at 32760 tokens."""
+    w = synth.WAN14B_480P
+    p = synth.make_block_weights(w)
+    _, x = synth.make_latents(w)
+    P = params_to_device(p, w.dtype)
+    X = up(x, tdtype(w.dtype))
+    all_idx = torch.arange(w.L, dtype=torch.int32, device=device())
+    ys_all = api.block_partial(P, X, all_idx, w.L, w.H).clone()
+    rng = np.random.default_rng(9)
+    sub = np.sort(rng.choice(w.L, w.K, replace=False)).astype(np.int32)
+    ys_sub = api.block_partial(P, X, up(sub), w.K, w.H)
+    torch.cuda.synchronize()
+    a = down(ys_all)[sub]
+    b = down(ys_sub)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+# --------------------------------------------------------------- whole step
+
+@pytest.mark.parametrize("w", [synth.TINY, RAGGED, synth.SMALL], ids=lambda w: w.name)
+def test_cached_step_end_to_end(w):
+    say(f"step {w.name}")
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w) if w is not RAGGED else np.array([0.3, 1.0, 0.0], np.float32)
+    o_init = OST.init_step(p, xref, w.H, w.dtype)
+    o_step = OST.cached_step(p, x, o_init["cache"], fw, w.N, w.H, w.K, w.dtype)
+    dt = tdtype(w.dtype)
+    P = params_to_device(p, w.dtype)
+    blk = api.CachedBlock(P, w.H, w.L, w.D, device(), dt)
+    blk.init(up(xref, dt))
+    y = blk.step(up(x, dt), up(fw), w.N, k=w.K)
+    torch.cuda.synchronize()
+    gi = down(blk.sel.idx)[: w.K]
+    check_selection(gi, o_step["idx"], o_step["s"], w.K)
+    same = np.array_equal(gi, o_step["idx"])
+    gy = down(y)
+    tol = TOL_F32_ABS if w.dtype == "f32" else TOL_BF16_ABS
+    if same:
+        check_block(down(blk.y_sel)[: w.K], o_step["y_sel"], w.dtype, f"{w.name}/step y_sel")
+    # reused rows: each side dequantizes its own cache; allow the block tolerance,
+    # one quantization step of either cache, and the final cast
+    rest = np.setdiff1d(np.arange(w.L), gi)
+    sc = np.maximum(down(blk.scale)[rest], o_step["cache"][2][rest])[:, None]
+    cast = np.abs(o_step["y"][rest]) * (2.0 ** -8 if w.dtype == "bf16" else 2.0 ** -23)
+    err = np.abs(gy[rest].astype(np.float64) - o_step["y"][rest])
+    assert (err <= tol + sc + cast).all(), float((err - (tol + sc + cast)).max())
+
+
+def test_cached_step_deterministic():
+    w = synth.SMALL
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w)
+    dt = tdtype(w.dtype)
+    P = params_to_device(p, w.dtype)
+    outs = []
+    for _ in range(2):
+        blk = api.CachedBlock(P, w.H, w.L, w.D, device(), dt)
+        blk.init(up(xref, dt))
+        y = blk.step(up(x, dt), up(fw), w.N, ratio=w.ratio)
+        torch.cuda.synchronize()
+        outs.append([down(t).copy() for t in (blk.sel.idx[: w.K], blk.sel.mask, blk.codes,
+                                              blk.scale, y)])
+    for a, b in zip(*outs):
+        assert np.array_equal(_bits(a), _bits(b))
