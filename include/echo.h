@@ -143,8 +143,9 @@ int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref,
  * shift1, scale1, gate1, shift2, scale2, gate2.
  * x [L][D] in `dtype`; idx [n_sel] int32 in [0, L) (any order, repeats allowed);
  * y_sel [n_sel][D] fp32, row j = output of token idx[j].  n_sel = 0 is a no-op.
- * Supported: ECHO_BF16 with D/H == 128, D % 256 == 0, F % 256 == 0 (bf16
- * MFMA path); ECHO_F32 with D % 4 == 0, (D/H) % 4 == 0, D/H <= 128,
+ * Supported: ECHO_BF16 with D/H == 128, D % 256 == 0, F % 256 == 0 and
+ * L*D, F*D, n_sel*F each below 2^30 elements (bf16 MFMA path; other shapes
+ * return ECHO_EUNSUPPORTED); ECHO_F32 with D % 4 == 0, (D/H) % 4 == 0, D/H <= 128,
  * F % 4 == 0 (fp32 path for small shapes).  D <= 16384, F <= 65536.
  */
 typedef struct {

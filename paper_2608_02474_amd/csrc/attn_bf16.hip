@@ -87,23 +87,6 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 #define ECHO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
-// Direct global-to-LDS copy of 16 bytes per lane: lane i's bytes land at LDS
-// offset lds_base + 16 i (lds_base is wave-uniform and goes through M0).
-// Written as inline asm on purpose: issued through the compiler builtin, every
-// later LDS read of the kernel is preceded by a wait for ALL outstanding
-// copies (the compiler cannot tell the ring stages apart), which would make
-// each iteration wait for the tile it has just prefetched.  The kernel
-// orders the copies itself (s_waitcnt vmcnt + barrier before a stage is
-// read); M0 is not used by anything else in this kernel.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_copy16(const void* gsrc, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(gsrc), "s"(lds_base)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
 #define ECHO_LDS_V4(p) ((__attribute__((address_space(3))) v4i16*)(p))
 
 template <int QB, int WAVES, int MODE>
@@ -159,7 +142,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
   const bf16_t* kh = k + hoff;
   const bf16_t* vh = v + hoff;
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ECHO_LDS(smem)));
+  const uint32_t lds0 = lds_offset(smem);
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto issue_tile = [&](int t, int stage) __attribute__((always_inline)) {
     const int key0 = t * ATT_KT;
@@ -357,7 +340,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     auto iteration = [&](auto stage_c, int t) __attribute__((always_inline)) {
       constexpr int ST = decltype(stage_c)::value;
       constexpr int ST2 = (ST + 2) % ATT_NSTAGE;
-      __builtin_amdgcn_s_waitcnt(NLD * 2);  // this wave's loads of tile t have landed
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));  // this wave's loads of tile t have landed
       __syncthreads();
       if (t + 2 < nkt) issue_tile(t + 2, ST2);
       compute_s(std::integral_constant<int, ST>{}, sacc);
@@ -382,10 +365,10 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     const bool late = wave >= WAVES / 2;
     f32x16 sacc[2][QB];
     bf16x8 pf[QB][2][2];
-    __builtin_amdgcn_s_waitcnt(NLD * 2);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
     __syncthreads();
     if (late) {
-      __builtin_amdgcn_s_waitcnt(NLD * 2);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
       __syncthreads();
     }
     auto round = [&](auto stage_c, int t) __attribute__((always_inline)) {
@@ -395,11 +378,11 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       if (t + 2 < nkt) issue_tile(t + 2, ST2);
       if (t > 0) pv(std::integral_constant<int, STP>{}, pf);
       compute_s(std::integral_constant<int, ST>{}, sacc);
-      __builtin_amdgcn_s_waitcnt(NLD * 2);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
       __syncthreads();
       // phase B: vector pipe
       softmax(sacc, t * ATT_KT, pf);
-      __builtin_amdgcn_s_waitcnt(NLD * 2);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
       __syncthreads();
     };
     int t = 0;

@@ -91,4 +91,41 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
+// Direct global-to-LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane i's bytes land at LDS offset lds_base + 16 i; lds_base is wave-uniform
+// and goes through M0.  Written as inline asm on purpose: issued through the
+// compiler builtin, every later LDS read of a kernel is preceded by a wait for
+// ALL outstanding copies (the compiler cannot tell ring stages apart), so each
+// iteration would wait for the tile it has just prefetched.  Kernels that use
+// it order the copies themselves (s_waitcnt vmcnt + barrier before a stage is
+// read) and use M0 for nothing else.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_copy16(const void* gsrc, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gsrc), "s"(lds_base)
+               : "memory", "m0");
+}
+// The same copy with a wave-uniform 64-bit base in SGPRs and a 32-bit
+// unsigned per-lane byte offset (the saddr form): one VGPR per copy.
+__device__ __forceinline__ void lds_copy16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_base)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt immediate (gfx9 layout) that waits until at most n vector-memory
+// operations of this wave are outstanding, and for all LDS/scalar operations
+// (vmcnt bits [3:0] and [15:14]; expcnt and lgkmcnt 0).
+__host__ __device__ constexpr int waitcnt_vm(int n) { return (n & 15) | (((n >> 4) & 3) << 14); }
+
+// LDS byte offset of a __shared__ object
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  // a C-style cast is the address-space conversion (generic -> LDS)
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)p));
+}
+
 }  // namespace echo

@@ -107,7 +107,10 @@ bool block_cfg_ok(const echo_block_cfg* c) {
 }
 bool block_supported(const echo_block_cfg* c) {
   const int dh = c->D / c->H;
-  if (c->dtype == ECHO_BF16) return dh == 128 && (c->D % 256) == 0 && (c->F % 256) == 0;
+  // bf16 GEMM tiles address their operands through 32-bit byte offsets
+  if (c->dtype == ECHO_BF16)
+    return dh == 128 && (c->D % 256) == 0 && (c->F % 256) == 0 &&
+           int64_t(c->L) * c->D < (int64_t(1) << 30) && int64_t(c->F) * c->D < (int64_t(1) << 30);
   return dh <= 128;
 }
 struct BlockWs {
@@ -224,6 +227,7 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
   if (!block_cfg_ok(cfg) || !weights_ok(w) || n_sel < 0) return ECHO_EINVAL;
   if (!block_supported(cfg)) return ECHO_EUNSUPPORTED;
   if (n_sel == 0) return ECHO_OK;
+  if (cfg->dtype == ECHO_BF16 && int64_t(n_sel) * cfg->F >= (int64_t(1) << 30)) return ECHO_EUNSUPPORTED;
   if (!ok_ptr(x) || !ok_ptr(idx) || !ok_ptr(y_sel)) return ECHO_EINVAL;
   const size_t need = block_ws_layout(cfg, n_sel, nullptr).bytes;
   if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
@@ -238,12 +242,12 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
     typedef const bf16_t* P;
     GemmBf16Args g{};
     // q = a[idx] Wq^T + bq
-    g = GemmBf16Args{static_cast<P>(ws.a), D, idx, static_cast<P>(w->wq), static_cast<P>(w->wq), D, D,
+    g = GemmBf16Args{static_cast<P>(ws.a), D, idx, L, static_cast<P>(w->wq), static_cast<P>(w->wq), D, D,
                      static_cast<P>(w->bq), static_cast<P>(w->bq), n, D, D, ws.q, D,
                      nullptr, nullptr, 0, nullptr, 0};
     if ((e = launch_gemm_bf16("gemm_q_bf16", 0, g, st)) != hipSuccess) return device_status(e);
     // [k | v] = a [Wk; Wv]^T + [bk; bv], one N = 2D GEMM over all L rows
-    g = GemmBf16Args{static_cast<P>(ws.a), D, nullptr, static_cast<P>(w->wk), static_cast<P>(w->wv), D,
+    g = GemmBf16Args{static_cast<P>(ws.a), D, nullptr, L, static_cast<P>(w->wk), static_cast<P>(w->wv), D,
                      D, static_cast<P>(w->bk), static_cast<P>(w->bv), L, 2 * D, D, ws.kv, 2 * D,
                      nullptr, nullptr, 0, nullptr, 0};
     if ((e = launch_gemm_bf16("gemm_kv_bf16", 0, g, st)) != hipSuccess) return device_status(e);
@@ -252,7 +256,7 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
                               static_cast<bf16_t*>(ws.o), D, st)) != hipSuccess)
       return device_status(e);
     // x1 = x[idx] + gate1 * (o Wo^T + bo)
-    g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, static_cast<P>(w->wo), static_cast<P>(w->wo), D,
+    g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, n, static_cast<P>(w->wo), static_cast<P>(w->wo), D,
                      D, static_cast<P>(w->bo), static_cast<P>(w->bo), n, D, D, ws.x1, D,
                      mod + 2 * D, x, D, idx, 1};
     if ((e = launch_gemm_bf16("gemm_o_bf16", 2, g, st)) != hipSuccess) return device_status(e);
@@ -260,12 +264,12 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
         hipSuccess)
       return device_status(e);
     // h = GELU(b W1^T + b1)
-    g = GemmBf16Args{static_cast<P>(ws.b), D, nullptr, static_cast<P>(w->w1), static_cast<P>(w->w1), F,
+    g = GemmBf16Args{static_cast<P>(ws.b), D, nullptr, n, static_cast<P>(w->w1), static_cast<P>(w->w1), F,
                      D, static_cast<P>(w->b1), static_cast<P>(w->b1), n, F, D, ws.h, F,
                      nullptr, nullptr, 0, nullptr, 0};
     if ((e = launch_gemm_bf16("gemm_ffn_up_bf16", 1, g, st)) != hipSuccess) return device_status(e);
     // y_sel = x1 + gate2 * (h W2^T + b2)
-    g = GemmBf16Args{static_cast<P>(ws.h), F, nullptr, static_cast<P>(w->w2), static_cast<P>(w->w2), D,
+    g = GemmBf16Args{static_cast<P>(ws.h), F, nullptr, n, static_cast<P>(w->w2), static_cast<P>(w->w2), D,
                      F, static_cast<P>(w->b2), static_cast<P>(w->b2), n, D, F, y_sel, D,
                      mod + 5 * D, ws.x1, D, nullptr, 0};
     if ((e = launch_gemm_bf16("gemm_ffn_down_bf16", 2, g, st)) != hipSuccess) return device_status(e);

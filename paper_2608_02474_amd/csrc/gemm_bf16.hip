@@ -11,25 +11,45 @@
 // Both operands are K-contiguous, which is what the MFMA operand layout wants:
 // every lane feeds 8 consecutive k values (16 bytes).
 //
-// Tiling for gfx950: 256 x 256 output tile per 512-thread workgroup (8 waves
-// as 2 x 4, each wave 128 x 64 = 4 x 2 tiles of v_mfma_f32_32x32x16_bf16),
-// k-step 64, A and B tiles double-buffered in LDS (128 KB of the 160 KB), one
-// barrier per k-step.  LDS rows are 128 bytes; 16-byte chunks are XOR-swizzled
-// by the row index so that the 32 rows a wave reads at one k offset fall into
-// distinct bank groups.  Workgroup ids are remapped so that each XCD (blocks
-// are dealt round-robin to the 8 XCDs) owns a contiguous run of tiles, then
-// grouped 8 tile-rows at a time so a run shares A and B panels in its L2.
-// Requires N % 256 == 0 and K % 64 == 0; M is arbitrary (tail rows clamp their
-// loads and skip their stores).
+// Tiling for gfx950: a BM x BN output tile per workgroup of WM x WN waves,
+// each wave (BM/WM) x (BN/WN) as 32x32 blocks of v_mfma_f32_32x32x16_bf16,
+// k-step 64.  A and B tiles are copied straight from global memory into a
+// double-buffered LDS ring with direct global-to-LDS loads (no VGPR staging;
+// each lane fetches the 16-byte piece whose swizzled slot is its lane slot),
+// one barrier per k-step.  LDS rows are 128 bytes; the 16-byte chunk of row r
+// is XOR-swizzled by (r >> 1) & 7 so that the 16 rows one LDS cycle reads
+// (two rows per 256-byte bank window) hit 16 distinct bank groups.
+// Workgroup ids are remapped so that each XCD (blocks are dealt round-robin
+// to the 8 XCDs) owns a contiguous run of tiles, then grouped 8 tile-rows at
+// a time so a run shares A and B panels in its L2.
+// Requires N % BN == 0, n_split % BN == 0, K % BK == 0 and byte offsets of
+// A and B rows below 2^31; M is arbitrary (tail rows clamp their loads and
+// skip their stores).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
 
 namespace echo {
 
-constexpr int GBM = 256, GBN = 256, GBK = 64, GTHREADS = 512;
+// LDS rows hold BK bf16 (BK/8 chunks of 16 B).  The chunk of row r is
+// XOR-swizzled so that the 16 consecutive rows one LDS cycle serves (256
+// bytes = 2 rows of 128 B, or 4 rows of 64 B) land in 16 distinct bank groups.
+template <int BK>
+__device__ __forceinline__ int gslot(int row, int chunk) {
+  if (BK == 64) return chunk ^ ((row >> 1) & 7);
+  return chunk ^ ((row >> 2) & 3);
+}
 
-__device__ __forceinline__ int gswz(int row, int chunk) { return chunk ^ (row & 7); }
+// f(integral_constant<int, I>) for I = B .. E-1, unrolled at compile time
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // GELU with the tanh approximation, using 0.5 z (1 + tanh u) = z / (1 + e^{-2u}).
 __device__ __forceinline__ float gelu_tanh_fast(float z) {
@@ -37,15 +57,33 @@ __device__ __forceinline__ float gelu_tanh_fast(float z) {
   return z / (1.0f + __expf(-2.0f * u));
 }
 
-template <int EPI>
-__global__ void __launch_bounds__(GTHREADS, 1) gemm_bf16_nt(GemmBf16Args p) {
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (GBM + GBN) * GBK];
+template <int BM, int BN, int WM, int WN, int NS, int BK>
+struct GemmCfg {
+  static constexpr int kWaves = WM * WN;
+  static constexpr int kThreads = kWaves * 64;
+  static constexpr int kTM = BM / WM / 32;                 // 32x32 blocks per wave (rows)
+  static constexpr int kTN = BN / WN / 32;                 // (columns)
+  static constexpr int kRowBytes = BK * 2;
+  static constexpr int kRowsPerCopy = 1024 / kRowBytes;     // rows one 1 KB copy fills
+  static constexpr int kStageBytes = (BM + BN) * kRowBytes;  // A + B tiles
+  static constexpr int kCopies = (BM + BN) / kRowsPerCopy / kWaves;  // per wave per k-step
+  static_assert(BK == 32 || BK == 64, "k-step of 32 or 64");
+  static_assert((BM + BN) % (kRowsPerCopy * kWaves) == 0, "copies split evenly over the waves");
+  static_assert(BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tile of 32x32 blocks");
+  static_assert(NS >= 2 && NS <= 5 && NS * kStageBytes <= 160 * 1024, "LDS ring fits");
+};
+
+template <int BM, int BN, int WM, int WN, int NS, int BK, int EPI>
+__global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) {
+  typedef GemmCfg<BM, BN, WM, WN, NS, BK> C;
+  constexpr int CPR = BK / 8;  // 16-byte chunks per row
+  __shared__ __attribute__((aligned(1024))) char smem[NS * C::kStageBytes];
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave, l32 = lane & 31, hi = lane >> 5;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
 
   // ---- tile id: XCD-contiguous runs, then groups of 8 tile-rows
-  const int tm = (p.M + GBM - 1) / GBM, tn = p.N / GBN, tiles = tm * tn;
+  const int tm = (p.M + BM - 1) / BM, tn = p.N / BN, tiles = tm * tn;
   int pid = blockIdx.x;
   {
     const int q = tiles / 8, r = tiles % 8, xcd = pid % 8, loc = pid / 8;
@@ -57,139 +95,259 @@ __global__ void __launch_bounds__(GTHREADS, 1) gemm_bf16_nt(GemmBf16Args p) {
   const int gm = (tm - first_m) < GROUP ? (tm - first_m) : GROUP;
   const int tile_m = first_m + (pid % group_size) % gm;
   const int tile_n = (pid % group_size) / gm;
-  const int m0 = tile_m * GBM, n0 = tile_n * GBN;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
 
-  // ---- per-thread global source rows and LDS destinations (4 A + 4 B chunks per k-step)
-  const bf16_t* asrc[4];
-  const bf16_t* bsrc[4];
-  int adst[4];
+  // ---- copy plan: copy c of this wave fills kRowsPerCopy tile rows (1 KB) of
+  // A (rows < BM) or B; the lane lands in row kRowsPerCopy * idx + lane / CPR,
+  // slot lane % CPR.  The lane keeps a 32-bit byte offset into its matrix; the
+  // matrix base (advanced by one k-step per iteration) is wave-uniform.
+  uint32_t voff[C::kCopies];
+  bool is_a[C::kCopies];
+  uint32_t dst[C::kCopies];
+  const uint32_t lds0 = lds_offset(smem);
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const bf16_t* b_base = n0 < p.n_split ? p.B0 : p.B1;  // BN divides n_split
+  const int n_off = n0 < p.n_split ? n0 : n0 - p.n_split;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = tid + GTHREADS * i;
-    const int row = id >> 3, ch = id & 7;
-    int m = m0 + row;
-    m = m < p.M ? m : p.M - 1;
-    const int64_t ar = p.a_rows ? p.a_rows[m] : m;
-    asrc[i] = p.A + ar * p.lda + ch * 8;
-    const int n = n0 + row;
-    bsrc[i] = (n < p.n_split ? p.B0 + static_cast<int64_t>(n) * p.ldb
-                             : p.B1 + static_cast<int64_t>(n - p.n_split) * p.ldb) + ch * 8;
-    adst[i] = row * GBK + gswz(row, ch) * 8;
+  for (int c = 0; c < C::kCopies; ++c) {
+    const int idx = wave_u + C::kWaves * c;  // 1 KB block index within the stage
+    const int row = C::kRowsPerCopy * idx + lane / CPR;  // row of the (A ++ B) stage
+    const int chunk = gslot<BK>(row, lane % CPR);       // logical chunk in this lane's slot
+    is_a[c] = C::kRowsPerCopy * idx < BM;
+    if (is_a[c]) {
+      int m = m0 + row;
+      m = m < p.M ? m : p.M - 1;
+      const uint32_t ar = p.a_rows ? static_cast<uint32_t>(p.a_rows[m]) : static_cast<uint32_t>(m);
+      voff[c] = (ar * static_cast<uint32_t>(p.lda) + chunk * 8) * 2u;
+    } else {
+      const uint32_t n = n_off + row - BM;
+      voff[c] = (n * static_cast<uint32_t>(p.ldb) + chunk * 8) * 2u;
+    }
+    dst[c] = lds0 + idx * 1024;
+  }
+  auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
+    const bf16_t* sa = p.A + static_cast<int64_t>(kt) * BK;
+    const bf16_t* sb = b_base + static_cast<int64_t>(kt) * BK;
+#pragma unroll
+    for (int c = 0; c < C::kCopies; ++c)
+      lds_copy16_s(is_a[c] ? sa : sb, voff[c], dst[c] + stage * C::kStageBytes);
+  };
+  // refill source of the running k-step (set once per k-step)
+  const bf16_t* fill_a = p.A;
+  const bf16_t* fill_b = b_base;
+  uint32_t fill_off = 0;
+  auto issue_one = [&](int c) __attribute__((always_inline)) {
+    lds_copy16_s(is_a[c] ? fill_a : fill_b, voff[c], dst[c] + fill_off);
+  };
+
+  // ---- fragment read offsets (bytes within a stage): k16-step s reads chunk 2s + hi
+  constexpr int KS = BK / 16;  // k16-steps per k-step
+  int a_rd[KS], b_rd[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int ra = wm * (BM / WM) + l32;  // + i * 32 rows: same swizzle, folded into the offset
+    const int rb = BM + wn * (BN / WN) + l32;
+    a_rd[s] = ra * C::kRowBytes + gslot<BK>(ra, 2 * s + hi) * 16;
+    b_rd[s] = rb * C::kRowBytes + gslot<BK>(rb, 2 * s + hi) * 16;
   }
 
-  f32x16 acc[4][2];
+  f32x16 acc[C::kTM][C::kTN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::kTM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < C::kTN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  uint4 ra[4], rb[4];
-  const int nk = p.K / GBK;
+  // Fragments of two k16-steps live at once: step s+1 is read from LDS while
+  // the MFMAs of step s run.  sched_barrier pins that order (left alone, the
+  // scheduler hoists every read of a k-step above its MFMAs and runs out of
+  // registers).
+  bf16x8 fa[2][C::kTM], fb[2][C::kTN];
+  auto load = [&](auto set_c, int stage, int s) __attribute__((always_inline)) {
+    constexpr int SET = decltype(set_c)::value;
+    const char* base = smem + stage * C::kStageBytes;  // stage is wave-uniform, not unrolled
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = ldg16(asrc[i]);
-    rb[i] = ldg16(bsrc[i]);
-  }
-  {
-    bf16_t* As = smem;
-    bf16_t* Bs = smem + GBM * GBK;
+    for (int i = 0; i < C::kTM; ++i)
+      fa[SET][i] = *reinterpret_cast<const bf16x8*>(base + a_rd[s] + i * 32 * C::kRowBytes);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(As + adst[i]) = ra[i];
-      *reinterpret_cast<uint4*>(Bs + adst[i]) = rb[i];
-    }
-  }
+    for (int j = 0; j < C::kTN; ++j)
+      fb[SET][j] = *reinterpret_cast<const bf16x8*>(base + b_rd[s] + j * 32 * C::kRowBytes);
+  };
+  // MFMAs of one fragment set over accumulator rows [I0, I1), with the
+  // refill copies [Q0, Q1) spread evenly between them (group G of a k-step
+  // carries copies [G * kPerGroup, (G + 1) * kPerGroup)).
+  constexpr int kPerGroup = (C::kCopies + KS - 1) / KS;
+  auto mma = [&](auto set_c, auto i0_c, auto i1_c, auto g_c) __attribute__((always_inline)) {
+    constexpr int SET = decltype(set_c)::value;
+    constexpr int IA = decltype(i0_c)::value, IB = decltype(i1_c)::value, G = decltype(g_c)::value;
+    constexpr int NM = (IB - IA) * C::kTN;
+    constexpr int Q0 = G * kPerGroup < C::kCopies ? G * kPerGroup : C::kCopies;
+    constexpr int Q1 = Q0 + kPerGroup < C::kCopies ? Q0 + kPerGroup : C::kCopies;
+    constexpr int NQ = Q1 - Q0;
+#pragma unroll
+    for (int i = IA; i < IB; ++i)
+#pragma unroll
+      for (int j = 0; j < C::kTN; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[SET][i], fb[SET][j], acc[i][j], 0, 0, 0);
+        if constexpr (NQ > 0) {
+          const int t = (i - IA) * C::kTN + j;
+#pragma unroll
+          for (int q = 0; q < NQ; ++q)
+            if (t == q * NM / NQ) issue_one(Q0 + q);
+        }
+      }
+  };
+  typedef std::integral_constant<int, 0> I0;
+  typedef std::integral_constant<int, 1> I1;
+  typedef std::integral_constant<int, C::kTM / 2> IH;
+  typedef std::integral_constant<int, C::kTM> IM;
+  typedef std::integral_constant<int, (KS - 1) & 1> ILAST;
+
+  // NS-stage ring: k-step kt reads stage kt % NS while kt+1 .. kt+NS-1 are
+  // in flight.  The barrier of k-step kt sits inside its last MFMA group:
+  // before it, every wave has issued all its reads of stage kt % NS (which
+  // k-step kt+1 refills with kt+NS) and waited until at most its copies of
+  // the newest NS-2 k-steps are outstanding, so after it stage (kt+1) % NS is
+  // complete and its first fragments are read under the remaining MFMAs.
+  const int nk = p.K / BK;
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s, s);
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm((NS - 2) * C::kCopies));  // k-step 0 complete
   __syncthreads();
-
+  load(I0{}, 0, 0);
+  int stage = 0;
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      const int64_t ko = static_cast<int64_t>(kt + 1) * GBK;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra[i] = ldg16(asrc[i] + ko);
-        rb[i] = ldg16(bsrc[i] + ko);
-      }
-    }
-    const bf16_t* As = smem + cur * (GBM + GBN) * GBK;
-    const bf16_t* Bs = As + GBM * GBK;
-#pragma unroll
-    for (int s = 0; s < GBK / 16; ++s) {
-      const int ch = 2 * s + hi;
-      bf16x8 a[4], b[2];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm * 128 + i * 32 + l32;
-        a[i] = *reinterpret_cast<const bf16x8*>(As + row * GBK + gswz(row, ch) * 8);
-      }
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int row = wn * 64 + j * 32 + l32;
-        b[j] = *reinterpret_cast<const bf16x8*>(Bs + row * GBK + gswz(row, ch) * 8);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) {
-      bf16_t* An = smem + (cur ^ 1) * (GBM + GBN) * GBK;
-      bf16_t* Bn = An + GBM * GBK;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *reinterpret_cast<uint4*>(An + adst[i]) = ra[i];
-        *reinterpret_cast<uint4*>(Bn + adst[i]) = rb[i];
-      }
-    }
+    const int next = stage + 1 == NS ? 0 : stage + 1;
+    const int fill = stage == 0 ? NS - 1 : stage - 1;
+    // k-step kt + NS - 1 goes to the stage read at kt - 1; past the end the
+    // last k-step is fetched again (in bounds, never read) so that every
+    // k-step issues the same copies and the wait below is uniform.
+    const int kf = kt + NS - 1 < nk ? kt + NS - 1 : nk - 1;
+    fill_a = p.A + static_cast<int64_t>(kf) * BK;
+    fill_b = b_base + static_cast<int64_t>(kf) * BK;
+    fill_off = fill * C::kStageBytes;
+    static_for<0, KS - 1>([&](auto s_c) __attribute__((always_inline)) {
+      constexpr int S = decltype(s_c)::value;
+      __builtin_amdgcn_sched_barrier(0);
+      load(std::integral_constant<int, (S + 1) & 1>{}, stage, S + 1);
+      mma(std::integral_constant<int, S & 1>{}, I0{}, IM{}, s_c);
+    });
+    __builtin_amdgcn_sched_barrier(0);
+    mma(ILAST{}, I0{}, IH{}, std::integral_constant<int, KS - 1>{});
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((NS - 2) * C::kCopies));
     __syncthreads();
+    if (kt + 1 < nk) load(I0{}, next, 0);
+    mma(ILAST{}, IH{}, IM{}, std::integral_constant<int, KS>{});
+    __builtin_amdgcn_sched_barrier(0);
+    stage = next;
   }
+  __builtin_amdgcn_s_waitcnt(0);  // refetched k-steps still landing in LDS
 
-  // ---- epilogue.  32x32 accumulator layout: lane holds column l32 and rows
-  // 8*(r/4) + 4*hi + r%4 for register r.
+  // ---- epilogue.  The 32x32 accumulator layout (lane holds column l32 and
+  // rows 8*(r/4) + 4*hi + r%4 of register r) is turned into row-contiguous
+  // pieces through LDS: each wave stages one 32-row slab of its tile at a
+  // time in a private region and reads it back as 4 consecutive columns per
+  // lane, so bias, gate and residual are read and the output written 8-16
+  // bytes per lane.  Staged rows are padded by 8 floats: the two half-waves
+  // (rows r and r+4) then write disjoint bank halves.
+  constexpr int WCOLS = C::kTN * 32;        // columns of a wave tile
+  constexpr int EP_LD = WCOLS + 8;          // staged row stride (floats)
+  constexpr int LPR = WCOLS / 4;            // lanes per staged row
+  constexpr int RPI = kWave / LPR;          // rows per read instruction
+  static_assert(C::kWaves * 32 * EP_LD * 4 <= NS * C::kStageBytes, "epilogue staging fits the ring");
+  __syncthreads();  // every wave is done with the ring
+  float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EP_LD;
+  const int c_l = (lane % LPR) * 4;                   // first of this lane's 4 columns
+  const int col = n0 + wn * (BN / WN) + c_l;           // global column (4 | col)
+  const bf16_t* bias_p = col < p.n_split ? p.bias0 + col : p.bias1 + (col - p.n_split);
+  float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  {
+    const uint2 bb = *reinterpret_cast<const uint2*>(bias_p);
+    bias[0] = __uint_as_float(bb.x << 16);
+    bias[1] = __uint_as_float(bb.x & 0xffff0000u);
+    bias[2] = __uint_as_float(bb.y << 16);
+    bias[3] = __uint_as_float(bb.y & 0xffff0000u);
+    if (EPI == EPI_GATE_RES) {
+      const float4 g = *reinterpret_cast<const float4*>(p.gate + col);
+      gate[0] = g.x; gate[1] = g.y; gate[2] = g.z; gate[3] = g.w;
+    }
+  }
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int col = n0 + wn * 64 + j * 32 + l32;
-    const float bias = bf16_to_f32(col < p.n_split ? p.bias0[col] : p.bias1[col - p.n_split]);
-    const float gate = (EPI == EPI_GATE_RES) ? p.gate[col] : 0.0f;
+  for (int i = 0; i < C::kTM; ++i) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int j = 0; j < C::kTN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
-        if (row >= p.M) continue;
-        const float v = acc[i][j][r] + bias;
-        if (EPI == EPI_BIAS) {
-          static_cast<bf16_t*>(p.C)[static_cast<int64_t>(row) * p.ldc + col] = f32_to_bf16(v);
-        } else if (EPI == EPI_GELU) {
-          static_cast<bf16_t*>(p.C)[static_cast<int64_t>(row) * p.ldc + col] =
-              f32_to_bf16(gelu_tanh_fast(v));
-        } else {
+      for (int r = 0; r < 16; ++r)
+        ep[(8 * (r >> 2) + 4 * hi + (r & 3)) * EP_LD + j * 32 + l32] = acc[i][j][r];
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(63));  // this wave's staged slab is in LDS
+#pragma unroll
+    for (int q = 0; q < 32 / RPI; ++q) {
+      const int r_l = q * RPI + lane / LPR;
+      const int row = m0 + wm * (BM / WM) + i * 32 + r_l;
+      const float4 a4 = *reinterpret_cast<const float4*>(ep + r_l * EP_LD + c_l);
+      float v[4] = {a4.x + bias[0], a4.y + bias[1], a4.z + bias[2], a4.w + bias[3]};
+      if (row < p.M) {
+        if (EPI == EPI_GATE_RES) {
           const int64_t rr = p.res_rows ? p.res_rows[row] : row;
-          const float res = p.res_bf16
-                                ? bf16_to_f32(static_cast<const bf16_t*>(p.res)[rr * p.ldr + col])
-                                : static_cast<const float*>(p.res)[rr * p.ldr + col];
-          static_cast<float*>(p.C)[static_cast<int64_t>(row) * p.ldc + col] = res + gate * v;
+          float res[4];
+          if (p.res_bf16) {
+            const uint2 rb = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
+            res[0] = __uint_as_float(rb.x << 16);
+            res[1] = __uint_as_float(rb.x & 0xffff0000u);
+            res[2] = __uint_as_float(rb.y << 16);
+            res[3] = __uint_as_float(rb.y & 0xffff0000u);
+          } else {
+            const float4 rf = *reinterpret_cast<const float4*>(static_cast<const float*>(p.res) + rr * p.ldr + col);
+            res[0] = rf.x; res[1] = rf.y; res[2] = rf.z; res[3] = rf.w;
+          }
+          float4 o;
+          o.x = res[0] + gate[0] * v[0];
+          o.y = res[1] + gate[1] * v[1];
+          o.z = res[2] + gate[2] * v[2];
+          o.w = res[3] + gate[3] * v[3];
+          *reinterpret_cast<float4*>(static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
+        } else {
+          if (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_fast(v[e]);
+          }
+          uint2 o;
+          o.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+          o.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
         }
       }
     }
   }
 }
 
-hipError_t launch_gemm_bf16(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream) {
-  if (a.M <= 0) return hipSuccess;
-  const int tiles = ((a.M + GBM - 1) / GBM) * (a.N / GBN);
-  const dim3 grid(tiles), block(GTHREADS);
+template <int BM, int BN, int WM, int WN, int NS, int BK>
+hipError_t launch_gemm_tile(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream) {
+  typedef GemmCfg<BM, BN, WM, WN, NS, BK> C;
+  if (a.N % BN != 0 || (a.n_split < a.N && a.n_split % BN != 0) || a.K % BK != 0)
+    return hipErrorInvalidValue;
+  const int tiles = ((a.M + BM - 1) / BM) * (a.N / BN);
+  const dim3 grid(tiles), block(C::kThreads);
   switch (epi) {
     case EPI_BIAS:
-      return ECHO_LAUNCH(name, gemm_bf16_nt<EPI_BIAS>, grid, block, 0, stream, a);
+      return ECHO_LAUNCH(name, (gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI_BIAS>), grid, block, 0, stream, a);
     case EPI_GELU:
-      return ECHO_LAUNCH(name, gemm_bf16_nt<EPI_GELU>, grid, block, 0, stream, a);
+      return ECHO_LAUNCH(name, (gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI_GELU>), grid, block, 0, stream, a);
     default:
-      return ECHO_LAUNCH(name, gemm_bf16_nt<EPI_GATE_RES>, grid, block, 0, stream, a);
+      return ECHO_LAUNCH(name, (gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI_GATE_RES>), grid, block, 0, stream, a);
   }
+}
+
+hipError_t launch_gemm_bf16(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream) {
+  if (a.M <= 0) return hipSuccess;
+  // the tile loads address A and B through 32-bit byte offsets
+  const int64_t lim = int64_t(1) << 31;
+  if (a.a_nrows <= 0 || a.a_nrows * a.lda * 2 >= lim || int64_t(a.N) * a.ldb * 2 >= lim)
+    return hipErrorInvalidValue;
+  return launch_gemm_tile<256, 256, 2, 4, 4, 32>(name, epi, a, stream);
 }
 
 }  // namespace echo

@@ -16,6 +16,7 @@ struct GemmBf16Args {
   const bf16_t* A;
   int64_t lda;
   const int32_t* a_rows;    // optional: A row of output row m is a_rows[m]
+  int64_t a_nrows;          // rows of A (every row index is below it)
   const bf16_t* B0;
   const bf16_t* B1;         // rows n >= n_split come from B1 (row n - n_split)
   int n_split;
