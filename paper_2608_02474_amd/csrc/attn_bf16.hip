@@ -13,8 +13,8 @@
 //     query fragments stay in registers for the whole key loop; K rows enter
 //     the MFMA in a permuted order (bits 2 and 3 of the row index swapped) so
 //     that each lane's accumulators hold 8 consecutive keys per 16-key step.
-//   * S of tile t+1 is issued before the softmax of tile t, so the MFMA pipe
-//     works while the VALU runs exp/max/sum of the previous tile.
+//   * K and V^T fragments flow through a small register ring, each read
+//     issued a fixed number of MFMAs ahead of its use.
 //   * softmax per lane: a lane owns one query per block (its accumulator
 //     column) and half of the tile's keys; the row max uses one
 //     v_permlane32_swap.  The scale is folded into one FMA before exp2;
@@ -43,21 +43,18 @@ constexpr int ATT_TILE_BYTES = ATT_KT * ATT_DH * 2;  // one K or V tile: 16 KB
 constexpr int ATT_STAGE_BYTES = 2 * ATT_TILE_BYTES;  // K + V
 constexpr int ATT_OS_STRIDE = ATT_DH + 8;            // output staging row (bf16)
 constexpr float ATT_RESCALE_LOG2 = 8.0f;             // lazy-rescale headroom (log2 units)
+constexpr int ATT_RING = 2;                          // LDS fragment reads in flight per wave
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// MODE 0: per tile, barrier -> S -> softmax -> PV.
-// MODE 1: S of the next tile issued before the softmax of this one.
-// MODE 2: ping-pong.  The waves split into two groups that run the same
-//         two-phase loop (phase A: PV of the previous tile + S of this tile on
-//         the MFMA pipe; phase B: softmax on the VALU) one phase apart, so on
-//         every SIMD one wave feeds the matrix pipe while the other runs exp.
-template <int QB, int WAVES, int MODE>
+// Per tile: barrier -> S -> softmax -> PV; the two waves of a SIMD overlap
+// each other's LDS latency and vector work.
+template <int QB, int WAVES>
 struct AttCfg {
   static constexpr int kThreads = WAVES * 64;
   static constexpr int kQ = WAVES * QB * 32;  // queries per workgroup
-  static constexpr int kStages = MODE == 2 ? 4 : 3;
+  static constexpr int kStages = 3;
   static constexpr int kLdsBytes = (kStages * ATT_STAGE_BYTES > kQ * ATT_OS_STRIDE * 2)
                                        ? kStages * ATT_STAGE_BYTES
                                        : kQ * ATT_OS_STRIDE * 2;
@@ -89,12 +86,12 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 #define ECHO_LDS_V4(p) ((__attribute__((address_space(3))) v4i16*)(p))
 
-template <int QB, int WAVES, int MODE>
+template <int QB, int WAVES>
 __global__ void __launch_bounds__(WAVES * 64, 1)
 attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k,
               const bf16_t* __restrict__ v, int64_t ldkv, int Mq, int L, int H, float scale_log2,
               bf16_t* __restrict__ out, int64_t ldo) {
-  typedef AttCfg<QB, WAVES, MODE> C;
+  typedef AttCfg<QB, WAVES> C;
   constexpr int ATT_NSTAGE = C::kStages;
   constexpr int NLD = 16 / WAVES;  // 1 KB direct-load instructions per wave per K (or V) tile
   static_assert(16 % WAVES == 0, "16 KB tiles split evenly over the waves");
@@ -206,43 +203,62 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
 
   const f32x16 zero16 = {};
+  // Fragments flow through a ring of ATT_RING registers: the read for step
+  // i + ATT_RING is issued right after the MFMA of step i has taken its
+  // operand, so every MFMA finds its fragment ATT_RING steps old.
   auto compute_s = [&](auto stage_c, f32x16(&sacc)[2][QB]) __attribute__((always_inline)) {
     constexpr int STAGE = decltype(stage_c)::value;
     const char* ks = smem + STAGE * ATT_STAGE_BYTES;
+    bf16x8 ring[ATT_RING];
+#pragma unroll
+    for (int i = 0; i < ATT_RING; ++i)
+      ring[i] = *reinterpret_cast<const bf16x8*>(ks + (i / 8) * 32 * 256 + k_rd[i % 8]);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {  // step i: key block kb = i / 8, k16-step s = i % 8
+      const int kb = i / 8, st = i % 8;
+      const bf16x8 a = ring[i % ATT_RING];
+#pragma unroll
+      for (int b = 0; b < QB; ++b)
+        sacc[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[b][st], st == 0 ? zero16 : sacc[kb][b], 0, 0, 0);
+      const int n = i + ATT_RING;
+      if (n < 16)
+        ring[i % ATT_RING] = *reinterpret_cast<const bf16x8*>(ks + (n / 8) * 32 * 256 + k_rd[n % 8]);
+      __builtin_amdgcn_sched_barrier(0);  // keep the reads ATT_RING steps ahead
+    }
+  };
+
+  // ---- softmax, in four parts so that the pipelined loop can place them apart
+  auto mask_tail = [&](f32x16(&sacc)[2][QB], int key0) __attribute__((always_inline)) {
+    // ragged last tile: keys past L get -inf
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + kb * 32 * 256 + k_rd[s]);
+      for (int r = 0; r < 16; ++r) {
+        const bool valid = key0 + kb * 32 + 16 * (r >> 3) + 8 * hi + (r & 7) < L;
 #pragma unroll
-        for (int b = 0; b < QB; ++b)
-          sacc[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              a, qf[b][s], s == 0 ? zero16 : sacc[kb][b], 0, 0, 0);
+        for (int b = 0; b < QB; ++b) sacc[kb][b][r] = valid ? sacc[kb][b][r] : -INFINITY;
       }
   };
-
-  auto softmax = [&](f32x16(&sacc)[2][QB], int key0, bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
-    if (key0 + ATT_KT > L) {  // ragged last tile: keys past L get -inf
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool valid = key0 + kb * 32 + 16 * (r >> 3) + 8 * hi + (r & 7) < L;
-#pragma unroll
-          for (int b = 0; b < QB; ++b) sacc[kb][b][r] = valid ? sacc[kb][b][r] : -INFINITY;
-        }
-    }
+  // tile maximum of each query (lane pair l, l^32 holds one query column)
+  auto tile_max = [&](const f32x16(&sacc)[2][QB], float(&mx)[QB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      float mx = -INFINITY;
+      float m = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][b][r]);
-      mx = pair_max(mx);
-      const bool grow = (mx - m_run[b]) * scale_log2 > ATT_RESCALE_LOG2;
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[kb][b][r]);
+      mx[b] = pair_max(m);
+    }
+  };
+  // lazy rescale: only rows whose maximum grows by more than 2^8 move their
+  // reference; the others keep it (alpha = 1, untouched)
+  auto update_max = [&](const float(&mx)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const bool grow = (mx[b] - m_run[b]) * scale_log2 > ATT_RESCALE_LOG2;
       if (__builtin_expect(__ballot(grow) != 0ull, 0)) {
-        const float m_new = grow ? mx : m_run[b];
+        const float m_new = grow ? mx[b] : m_run[b];
         const float alpha = grow ? __builtin_amdgcn_exp2f((m_run[b] - m_new) * scale_log2) : 1.0f;
         m_run[b] = m_new;
         l_run[b] *= alpha;
@@ -251,9 +267,14 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[b][d][r] *= alpha;
       }
+    }
+  };
+  // probabilities as bf16 MFMA operands; the row sum adds the same bf16
+  // values, two per v_dot2 (fp32 accumulation)
+  auto probs = [&](const f32x16(&sacc)[2][QB], bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
       const float neg_mc = -m_run[b] * scale_log2;
-      // the row sum adds the bf16 probabilities the PV product uses, two per
-      // v_dot2 (fp32 accumulation)
       const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
       float psum = 0.0f;
 #pragma unroll
@@ -273,24 +294,38 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       l_run[b] += psum;
     }
   };
+  auto softmax = [&](f32x16(&sacc)[2][QB], int key0, bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
+    if (key0 + ATT_KT > L) mask_tail(sacc, key0);
+    float mx[QB];
+    tile_max(sacc, mx);
+    update_max(mx);
+    probs(sacc, pf);
+  };
 
   auto pv = [&](auto stage_c, const bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
     constexpr int STAGE = decltype(stage_c)::value;
     const char* vs = smem + STAGE * ATT_STAGE_BYTES;
+    // step i: dh block d = i / 4, key block kb = (i / 2) % 2, 16-key half a = i % 2
+    auto read_v = [&](int i) __attribute__((always_inline)) {
+      const int d = i / 4, kb = (i / 2) % 2, a = i % 2;
+      const int step = (kb * 32 + 16 * a) * 256;
+      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][0]));
+      const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][1]));
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    bf16x8 ring[ATT_RING];
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
+    for (int i = 0; i < ATT_RING; ++i) ring[i] = read_v(i);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int i = 0; i < 16; ++i) {
+      const int d = i / 4, kb = (i / 2) % 2, a = i % 2;
+      const bf16x8 va = ring[i % ATT_RING];
 #pragma unroll
-        for (int a = 0; a < 2; ++a) {
-          const int step = (kb * 32 + 16 * a) * 256;
-          const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][0]));
-          const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][1]));
-          const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-          for (int b = 0; b < QB; ++b)
-            o[b][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[b][kb][a], o[b][d], 0, 0, 0);
-        }
+      for (int b = 0; b < QB; ++b)
+        o[b][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[b][kb][a], o[b][d], 0, 0, 0);
+      if (i + ATT_RING < 16) ring[i % ATT_RING] = read_v(i + ATT_RING);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
   auto softmax_pv = [&](auto stage_c, f32x16(&sacc)[2][QB], int key0) __attribute__((always_inline)) {
@@ -303,44 +338,17 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   issue_tile(0, 0);
   if (nkt > 1) issue_tile(1, 1);
 
-  if constexpr (MODE == 1) {
-    f32x16 sa[2][QB], sb[2][QB];
-    // prologue: tiles 0 and 1 in flight, S(0) computed
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    compute_s(std::integral_constant<int, 0>{}, sa);
-    // iteration t: S(t) is in `cur`, tile t sits in stage t%3 and tile t+1 is
-    // being loaded into stage (t+1)%3
-    auto iteration = [&](auto stage_c, int t, f32x16(&cur)[2][QB], f32x16(&nxt)[2][QB]) __attribute__((always_inline)) {
-      constexpr int ST = decltype(stage_c)::value;
-      constexpr int ST1 = (ST + 1) % ATT_NSTAGE, ST2 = (ST + 2) % ATT_NSTAGE;
-      __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of tile t+1 have landed
-      __syncthreads();                // ... everyone's; and stage (t+2)%3 is no longer read
-      if (t + 2 < nkt) issue_tile(t + 2, ST2);
-      if (t + 1 < nkt) compute_s(std::integral_constant<int, ST1>{}, nxt);
-      softmax_pv(std::integral_constant<int, ST>{}, cur, t * ATT_KT);
-    };
-    // stages cycle with period 3 and the S buffers with period 2: unroll by 6
-    for (int t = 0; t < nkt; t += 6) {
-      iteration(std::integral_constant<int, 0>{}, t, sa, sb);
-      if (t + 1 >= nkt) break;
-      iteration(std::integral_constant<int, 1>{}, t + 1, sb, sa);
-      if (t + 2 >= nkt) break;
-      iteration(std::integral_constant<int, 2>{}, t + 2, sa, sb);
-      if (t + 3 >= nkt) break;
-      iteration(std::integral_constant<int, 0>{}, t + 3, sb, sa);
-      if (t + 4 >= nkt) break;
-      iteration(std::integral_constant<int, 1>{}, t + 4, sa, sb);
-      if (t + 5 >= nkt) break;
-      iteration(std::integral_constant<int, 2>{}, t + 5, sb, sa);
-    }
-  } else if constexpr (MODE == 0) {
+  {
     // iteration t: tile t sits in stage t%3, tile t+1 is in flight
     f32x16 sacc[2][QB];
     auto iteration = [&](auto stage_c, int t) __attribute__((always_inline)) {
       constexpr int ST = decltype(stage_c)::value;
       constexpr int ST2 = (ST + 2) % ATT_NSTAGE;
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));  // this wave's loads of tile t have landed
+      // this wave's loads of tile t have landed (tile t+1, if any, may still be in flight)
+      if (t + 1 < nkt)
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
+      else
+        __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       if (t + 2 < nkt) issue_tile(t + 2, ST2);
       compute_s(std::integral_constant<int, ST>{}, sacc);
@@ -353,57 +361,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       if (t + 2 >= nkt) break;
       iteration(std::integral_constant<int, 2>{}, t + 2);
     }
-  } else {
-    // Ping-pong.  Group 1 (the upper half of the waves) runs one phase behind
-    // group 0.  Tile t lives in stage t%4: it is read by S(t) in phase A(t)
-    // and by PV(t) in phase A(t+1) of both groups, and is overwritten by tile
-    // t+4, issued in phase A(t+2).  Before every barrier a wave waits until
-    // at most its newest tile's loads are in flight; every wave issues at most
-    // one tile between two barriers, so every older tile is complete.  Both
-    // groups execute the same number of barriers: group 1 one extra at the
-    // start, group 0 one extra at the end.
-    const bool late = wave >= WAVES / 2;
-    f32x16 sacc[2][QB];
-    bf16x8 pf[QB][2][2];
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
-    __syncthreads();
-    if (late) {
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
-      __syncthreads();
-    }
-    auto round = [&](auto stage_c, int t) __attribute__((always_inline)) {
-      constexpr int ST = decltype(stage_c)::value;           // stage of tile t
-      constexpr int STP = (ST + 3) % 4, ST2 = (ST + 2) % 4;  // tiles t-1 and t+2
-      // phase A: matrix pipe
-      if (t + 2 < nkt) issue_tile(t + 2, ST2);
-      if (t > 0) pv(std::integral_constant<int, STP>{}, pf);
-      compute_s(std::integral_constant<int, ST>{}, sacc);
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
-      __syncthreads();
-      // phase B: vector pipe
-      softmax(sacc, t * ATT_KT, pf);
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
-      __syncthreads();
-    };
-    int t = 0;
-    for (; t + 4 <= nkt; t += 4) {
-      round(std::integral_constant<int, 0>{}, t);
-      round(std::integral_constant<int, 1>{}, t + 1);
-      round(std::integral_constant<int, 2>{}, t + 2);
-      round(std::integral_constant<int, 3>{}, t + 3);
-    }
-    // tail rounds (nkt % 4 of them) and the last PV
-    const int rem = nkt - t;
-    if (rem > 0) round(std::integral_constant<int, 0>{}, t);
-    if (rem > 1) round(std::integral_constant<int, 1>{}, t + 1);
-    if (rem > 2) round(std::integral_constant<int, 2>{}, t + 2);
-    switch ((nkt - 1) & 3) {  // stage of the last tile
-      case 0: pv(std::integral_constant<int, 0>{}, pf); break;
-      case 1: pv(std::integral_constant<int, 1>{}, pf); break;
-      case 2: pv(std::integral_constant<int, 2>{}, pf); break;
-      default: pv(std::integral_constant<int, 3>{}, pf); break;
-    }
-    if (!late) __syncthreads();
   }
 
   // normalise and write through LDS so that global stores are full 16-byte rows
@@ -433,22 +390,22 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
 }
 
-template <int QB, int WAVES, int MODE>
+template <int QB, int WAVES>
 hipError_t launch_attn_variant(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                                int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
                                hipStream_t stream) {
   if (Mq <= 0) return hipSuccess;
-  typedef AttCfg<QB, WAVES, MODE> C;
+  typedef AttCfg<QB, WAVES> C;
   const float scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(ATT_DH)));
   const int ntq = (Mq + C::kQ - 1) / C::kQ;
-  return ECHO_LAUNCH("attn_fwd_bf16", (attn_fwd_bf16<QB, WAVES, MODE>), dim3(ntq * H), dim3(C::kThreads), 0,
+  return ECHO_LAUNCH("attn_fwd_bf16", (attn_fwd_bf16<QB, WAVES>), dim3(ntq * H), dim3(C::kThreads), 0,
                      stream, q, ldq, k, v, ldkv, Mq, L, H, scale_log2, out, ldo);
 }
 
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
                             hipStream_t stream) {
-  return launch_attn_variant<1, 8, 0>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, stream);
+  return launch_attn_variant<1, 8>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, stream);
 }
 
 }  // namespace echo

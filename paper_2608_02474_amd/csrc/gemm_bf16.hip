@@ -199,7 +199,6 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
       }
   };
   typedef std::integral_constant<int, 0> I0;
-  typedef std::integral_constant<int, 1> I1;
   typedef std::integral_constant<int, C::kTM / 2> IH;
   typedef std::integral_constant<int, C::kTM> IM;
   typedef std::integral_constant<int, (KS - 1) & 1> ILAST;
