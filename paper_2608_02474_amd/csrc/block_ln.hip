@@ -1,10 +1,14 @@
 // Modulated LayerNorm of token rows (the adaLN "LN(z) * (1 + scale) + shift"
 // in front of attention and FFN of the DiT block, Sec. 3.3).
 //
-// One wave per row; the row is held in registers (8-element chunks), mean and
-// biased variance are reduced in fp32 with two passes over the registers, and
-// the modulated result is written in the output storage type.  Rows longer than
-// 512 * MAXC elements take the MAXC == 0 variant, which re-reads the row.
+// One wave per row; the row is held in registers (8-element chunks, all loads
+// issued before the first is used), mean and biased variance are reduced in
+// fp32 with two passes over the registers, and the modulated result is
+// written in the output storage type.  Every access, the modulation vectors
+// included, is a 16-byte vector load or store.  Rows longer than 512 * MAXC
+// elements take the MAXC == 0 variant, which re-reads the row.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
@@ -41,45 +45,58 @@ modln_rows(const Tin* __restrict__ x, int M, int D, const float* __restrict__ sh
   const int nch = D / 8;
   const float invD = 1.0f / static_cast<float>(D);
   if (MAXC > 0) {
+    // every load of the row is issued before any of them is used; lanes past
+    // the row end re-load its last chunk (in bounds) and add nothing
     constexpr int R = MAXC > 0 ? MAXC : 1;
-    float v[R][8];
-    float sum = 0.0f;
+    auto body = [&](auto full_c) __attribute__((always_inline)) {
+      constexpr bool FULL = decltype(full_c)::value;  // every lane owns R chunks
+      Raw8<Tin> raw[R];
 #pragma unroll
-    for (int u = 0; u < R; ++u) {
-      const int c = lane + u * kWave;
-      if (c < nch) {
-        ln_load8(xr + c * 8, v[u]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) sum += v[u][j];
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        raw[u].load(xr + (FULL || c < nch ? c : nch - 1) * 8);
       }
-    }
-    const float mean = wave_sum(sum) * invD;
-    float sq = 0.0f;
+      float sum = 0.0f;
 #pragma unroll
-    for (int u = 0; u < R; ++u) {
-      const int c = lane + u * kWave;
-      if (c < nch) {
+      for (int u = 0; u < R; ++u) {
+        float v[8];
+        raw[u].unpack(v);
+        const bool ok = FULL || lane + u * kWave < nch;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sum += ok ? v[j] : 0.0f;
+      }
+      const float mean = wave_sum(sum) * invD;
+      float sq = 0.0f;
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        float v[8];
+        raw[u].unpack(v);
+        const bool ok = FULL || lane + u * kWave < nch;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float d = v[u][j] - mean;
-          sq += d * d;
+          const float d = v[j] - mean;
+          sq += ok ? d * d : 0.0f;
         }
       }
-    }
-    const float rstd = 1.0f / sqrtf(wave_sum(sq) * invD + eps);
+      const float rstd = 1.0f / sqrtf(wave_sum(sq) * invD + eps);
 #pragma unroll
-    for (int u = 0; u < R; ++u) {
-      const int c = lane + u * kWave;
-      if (c < nch) {
-        float o[8];
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        if (FULL || c < nch) {
+          float v[8], o[8], sc[8], sh[8];
+          raw[u].unpack(v);
+          ln_load8(scale + c * 8, sc);
+          ln_load8(shift + c * 8, sh);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int col = c * 8 + j;
-          o[j] = (v[u][j] - mean) * rstd * (1.0f + scale[col]) + shift[col];
+          for (int j = 0; j < 8; ++j) o[j] = (v[j] - mean) * rstd * (1.0f + sc[j]) + sh[j];
+          ln_store8(orow + c * 8, o);
         }
-        ln_store8(orow + c * 8, o);
       }
-    }
+    };
+    if (nch == R * kWave)
+      body(std::integral_constant<bool, true>{});
+    else
+      body(std::integral_constant<bool, false>{});
   } else {
     float sum = 0.0f;
     for (int c = lane; c < nch; c += kWave) {
@@ -101,13 +118,12 @@ modln_rows(const Tin* __restrict__ x, int M, int D, const float* __restrict__ sh
     }
     const float rstd = 1.0f / sqrtf(wave_sum(sq) * invD + eps);
     for (int c = lane; c < nch; c += kWave) {
-      float v[8], o[8];
+      float v[8], o[8], sc[8], sh[8];
       ln_load8(xr + c * 8, v);
+      ln_load8(scale + c * 8, sc);
+      ln_load8(shift + c * 8, sh);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int col = c * 8 + j;
-        o[j] = (v[j] - mean) * rstd * (1.0f + scale[col]) + shift[col];
-      }
+      for (int j = 0; j < 8; ++j) o[j] = (v[j] - mean) * rstd * (1.0f + sc[j]) + sh[j];
       ln_store8(orow + c * 8, o);
     }
   }
@@ -123,9 +139,13 @@ static hipError_t launch_modln_t(const char* name, const Tin* x, int M, int D, c
   if (per_lane <= MC)                                                                          \
     return ECHO_LAUNCH(name, (modln_rows<Tin, Tout, MC>), grid, dim3(kLnThreads), 0, stream, x, \
                        M, D, shift, scale, eps, out);
+  ECHO_LN_CASE(1)
   ECHO_LN_CASE(2)
+  ECHO_LN_CASE(3)
   ECHO_LN_CASE(4)
+  ECHO_LN_CASE(6)
   ECHO_LN_CASE(8)
+  ECHO_LN_CASE(10)
   ECHO_LN_CASE(12)
   ECHO_LN_CASE(16)
 #undef ECHO_LN_CASE

@@ -8,11 +8,14 @@
 //                           := x_i, output := cast(y_sel[j]);
 //   waves [n_sel, n_sel+L)  row i = wave - n_sel, if mask[i] == 0: output :=
 //                           cast(xref_i + scale_i * code).
-// Rows are streamed with 16-byte loads/stores (8 elements per chunk); the
-// fresh row is held in registers between the absmax and the quantization.
+// Rows are streamed with 16-byte loads/stores (8 elements per chunk), every
+// load of a row issued before the first is used; the fresh row's y and x stay
+// in registers between the absmax and the quantization.
 // Every fp32 step is a separately rounded IEEE operation (no fused
 // multiply-add), so codes and reused rows are exactly the fp32 values the
 // definition gives.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
@@ -78,25 +81,39 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
     const float* ys = y_sel + g * D;
     const T* xi = x + i * D;
     constexpr int R = MAXC > 0 ? MAXC : 1;
-    float res[R][8];
+    Raw8<float> yraw[R];
+    Raw8<T> xraw[R];
     float amax = 0.0f;
     if (MAXC > 0) {
+      // all loads of the row first; lanes past the row end re-load its last
+      // chunk (in bounds) and contribute nothing
+      auto body = [&](auto full_c) __attribute__((always_inline)) {
+        constexpr bool FULL = decltype(full_c)::value;  // every lane owns R chunks
 #pragma unroll
-      for (int u = 0; u < R; ++u) {
-        const int c = lane + u * kWave;
-        if (c < nch) {
-          float yv[8], xv[8];
-          load8(ys + c * 8, yv);
-          load8(xi + c * 8, xv);
-          store8(y + i * D + c * 8, yv);           // fresh output, cast to storage type
-          copy8(xi + c * 8, xref + i * D + c * 8);  // reference := current input
+        for (int u = 0; u < R; ++u) {
+          const int c = lane + u * kWave;
+          const int cc = FULL || c < nch ? c : nch - 1;
+          yraw[u].load(ys + cc * 8);
+          xraw[u].load(xi + cc * 8);
+        }
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            res[u][j] = __fsub_rn(yv[j], xv[j]);
-            amax = fmaxf(amax, fabsf(res[u][j]));
+        for (int u = 0; u < R; ++u) {
+          const int c = lane + u * kWave;
+          if (FULL || c < nch) {
+            float yv[8], xv[8];
+            yraw[u].unpack(yv);
+            xraw[u].unpack(xv);
+            store8(y + i * D + c * 8, yv);      // fresh output, cast to storage type
+            xraw[u].store(xref + i * D + c * 8);  // reference := current input
+#pragma unroll
+            for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(__fsub_rn(yv[j], xv[j])));
           }
         }
-      }
+      };
+      if (nch == R * kWave)
+        body(std::integral_constant<bool, true>{});
+      else
+        body(std::integral_constant<bool, false>{});
     } else {
       for (int c = lane; c < nch; c += kWave) {
         float yv[8], xv[8];
@@ -114,7 +131,14 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
 #pragma unroll
       for (int u = 0; u < R; ++u) {
         const int c = lane + u * kWave;
-        if (c < nch) quantize8(res[u], inv, codes + i * D + c * 8);
+        if (c < nch) {
+          float yv[8], xv[8], r[8];
+          yraw[u].unpack(yv);
+          xraw[u].unpack(xv);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) r[j] = __fsub_rn(yv[j], xv[j]);  // the same residual as above
+          quantize8(r, inv, codes + i * D + c * 8);
+        }
       }
     } else {
       for (int c = lane; c < nch; c += kWave) {
@@ -133,18 +157,46 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
   const int64_t i = g - n_sel;
   if (i >= L || mask[i]) return;
   const float sc = scale[i];
-  for (int c = lane; c < nch; c += kWave) {
-    float r[8];
-    load8(xref + i * D + c * 8, r);
-    const uint2 cw = *reinterpret_cast<const uint2*>(codes + i * D + c * 8);
+  auto reuse8 = [&](const Raw8<T>& rr, uint2 cw, int c) __attribute__((always_inline)) {
+    float r[8], out[8];
+    rr.unpack(r);
     const uint32_t w[2] = {cw.x, cw.y};
-    float out[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int8_t q = static_cast<int8_t>((w[j / 4] >> (8 * (j % 4))) & 0xffu);
       out[j] = mul_add_unfused(sc, static_cast<float>(q), r[j]);
     }
     store8(y + i * D + c * 8, out);
+  };
+  if (MAXC > 0) {
+    constexpr int R = MAXC > 0 ? MAXC : 1;
+    auto body = [&](auto full_c) __attribute__((always_inline)) {
+      constexpr bool FULL = decltype(full_c)::value;
+      Raw8<T> rr[R];
+      uint2 cw[R];
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        const int cc = FULL || c < nch ? c : nch - 1;
+        rr[u].load(xref + i * D + cc * 8);
+        cw[u] = *reinterpret_cast<const uint2*>(codes + i * D + cc * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        if (FULL || c < nch) reuse8(rr[u], cw[u], c);
+      }
+    };
+    if (nch == R * kWave)
+      body(std::integral_constant<bool, true>{});
+    else
+      body(std::integral_constant<bool, false>{});
+  } else {
+    for (int c = lane; c < nch; c += kWave) {
+      Raw8<T> rr;
+      rr.load(xref + i * D + c * 8);
+      reuse8(rr, *reinterpret_cast<const uint2*>(codes + i * D + c * 8), c);
+    }
   }
 }
 
@@ -159,9 +211,13 @@ static hipError_t launch_cache_t(const char* name, const T* x, const int32_t* id
   if (per_lane <= MC)                                                                          \
     return ECHO_LAUNCH(name, (cache_update_rows<T, MC>), grid, dim3(kCacheThreads), 0, stream, \
                        x, idx, mask, n_sel, L, D, y_sel, xref, codes, scale, y);
+  ECHO_CACHE_CASE(1)
   ECHO_CACHE_CASE(2)
+  ECHO_CACHE_CASE(3)
   ECHO_CACHE_CASE(4)
+  ECHO_CACHE_CASE(6)
   ECHO_CACHE_CASE(8)
+  ECHO_CACHE_CASE(10)
   ECHO_CACHE_CASE(12)
   ECHO_CACHE_CASE(16)
 #undef ECHO_CACHE_CASE

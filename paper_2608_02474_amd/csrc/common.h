@@ -74,6 +74,25 @@ __device__ __forceinline__ void stg16(void* p, const uint4& v) {
   *reinterpret_cast<uint4*>(p) = v;
 }
 
+// 8 consecutive elements as raw 16-byte vectors (one for bf16, two for fp32),
+// so that a row's loads can all be issued before any of them is unpacked
+template <typename T> struct Raw8;
+template <> struct Raw8<bf16_t> {
+  uint4 v;
+  __device__ void load(const bf16_t* p) { v = ldg16(p); }
+  __device__ void store(bf16_t* p) const { stg16(p, v); }
+  __device__ void unpack(float* o) const { unpack16(v, o, static_cast<const bf16_t*>(nullptr)); }
+};
+template <> struct Raw8<float> {
+  uint4 v0, v1;
+  __device__ void load(const float* p) { v0 = ldg16(p); v1 = ldg16(p + 4); }
+  __device__ void store(float* p) const { stg16(p, v0); stg16(p + 4, v1); }
+  __device__ void unpack(float* o) const {
+    unpack16(v0, o, static_cast<const float*>(nullptr));
+    unpack16(v1, o + 4, static_cast<const float*>(nullptr));
+  }
+};
+
 // wave64 reductions (every lane gets the result)
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

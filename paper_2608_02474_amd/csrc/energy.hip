@@ -4,7 +4,8 @@
 // Kernel 1 (energy_frames): one workgroup per (segment, STFT frame).  The
 // windowed frame and a full-period twiddle table live in LDS in fp64; each
 // thread evaluates whole one-sided bins k directly from the DFT sum, writes
-// |X_k|^2 to LDS, and one thread per band sums its bins in ascending order.
+// |X_k|^2 and the bin's band to LDS, and one thread per band sums its bins in
+// ascending order.
 // This runs once per clip on ~10^2-10^3 frames, so a direct O(n_fft^2) DFT in
 // fp64 costs microseconds and keeps the result within fp64 rounding of the
 // definition; an FFT would save nothing measurable here.
@@ -16,7 +17,8 @@
 
 namespace echo {
 
-constexpr int kEnergyThreads = 256;
+constexpr int kEnergyThreads = 256;   // energy_reduce (power of two: tree reduction)
+constexpr int kFrameThreads = 512;    // energy_frames: one thread per one-sided bin up to n_fft 1022
 constexpr int kMaxFft = 2048;
 
 __device__ __forceinline__ int band_of_bin(int k, int n_fft, int sr, int n_bands) {
@@ -28,7 +30,7 @@ __device__ __forceinline__ int band_of_bin(int k, int n_fft, int sr, int n_bands
   return b < n_bands - 1 ? b : n_bands - 1;
 }
 
-__global__ void __launch_bounds__(kEnergyThreads)
+__global__ void __launch_bounds__(kFrameThreads)
 energy_frames(const float* __restrict__ audio, int64_t n_samples, int T, int n_fft, int hop,
               int n_bands, int sr, int max_frames, double* __restrict__ part) {
   extern __shared__ double lds[];
@@ -36,6 +38,7 @@ energy_frames(const float* __restrict__ audio, int64_t n_samples, int T, int n_f
   double* tc = lds + n_fft;         // [n_fft] cos(2 pi m / n_fft)
   double* ts = lds + 2 * n_fft;     // [n_fft] sin(2 pi m / n_fft)
   double* pw = lds + 3 * n_fft;     // [n_fft/2 + 1] |X_k|^2
+  int* bandof = reinterpret_cast<int*>(lds + 3 * n_fft + n_fft / 2 + 1);  // [n_fft/2 + 1] band of bin k
   const int t = blockIdx.y, f = blockIdx.x;
   const int64_t a = (static_cast<int64_t>(t) * n_samples) / T;
   const int64_t b = (static_cast<int64_t>(t + 1) * n_samples) / T;
@@ -69,12 +72,13 @@ energy_frames(const float* __restrict__ audio, int64_t n_samples, int T, int n_f
       if (m >= n_fft) m -= n_fft;
     }
     pw[k] = re * re + im * im;
+    bandof[k] = band_of_bin(k, n_fft, sr, n_bands);
   }
   __syncthreads();
   for (int band = threadIdx.x; band < n_bands; band += blockDim.x) {
-    double acc = 0.0;
+    double acc = 0.0;  // bins of the band in ascending order
     for (int k = 0; k < nbins; ++k)
-      if (band_of_bin(k, n_fft, sr, n_bands) == band) acc += pw[k];
+      if (bandof[k] == band) acc += pw[k];
     out[band] = acc;
   }
 }
@@ -120,8 +124,8 @@ hipError_t launch_energy(const float* audio, int64_t n_samples, int T, int sr, i
                          int n_bands, float* band_energy, float* frame_energy, float* frame_weight,
                          double* part, double* e_scratch, hipStream_t stream) {
   const int mf = energy_max_frames(n_samples, T, n_fft, hop);
-  const size_t lds = sizeof(double) * (3 * n_fft + n_fft / 2 + 1);
-  hipError_t e = ECHO_LAUNCH("energy_frames", energy_frames, dim3(mf, T), dim3(kEnergyThreads), lds,
+  const size_t lds = sizeof(double) * (3 * n_fft + n_fft / 2 + 1) + sizeof(int) * (n_fft / 2 + 1);
+  hipError_t e = ECHO_LAUNCH("energy_frames", energy_frames, dim3(mf, T), dim3(kFrameThreads), lds,
                              stream, audio, n_samples, T, n_fft, hop, n_bands, sr, mf, part);
   if (e != hipSuccess) return e;
   return ECHO_LAUNCH("energy_reduce", energy_reduce, dim3(1), dim3(kEnergyThreads), 0, stream, part, T,

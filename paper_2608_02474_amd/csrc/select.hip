@@ -1,11 +1,12 @@
 // Saliency and recompute selection (Sec. 3.1 Eq. 1, applied per token against
 // its cached input; Sec. 3.3 saliency mask with k = ceil(r L) tokens).
 //
-// saliency_rows: one wave per token row streams x and xref with 16-byte loads
-//   and accumulates |x - xref| and |xref| in fp64 (exact per-element
-//   differences, so only the summation order differs from the definition).
+// saliency_rows: one wave per token row loads x and xref with 16-byte loads
+//   (all of a lane's loads issued before the first is used) and accumulates
+//   |x - xref| and |xref| in fp64 (exact per-element differences, so only the
+//   summation order differs from the definition).
 //   Writes s_i = fp32(w_frame * num / (den + xi)) plus num/den for the step sum.
-// select_rows: one 1024-thread workgroup
+// select_rows: one 1024-thread workgroup, the keys held in registers
 //   (1) step-level Eq. 1 sum in a fixed order (deterministic);
 //   (2) top-K threshold key by 4-pass 8-bit radix select over order-preserving
 //       uint32 keys (histograms in LDS);
@@ -24,7 +25,9 @@ constexpr int kSalThreads = 256;
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
 
-template <typename T>
+// MAXC > 0: a lane's MAXC chunks of 8 elements of x and xref are all loaded
+// before any is used (D <= 512 MAXC); MAXC == 0 streams the row (any D).
+template <typename T, int MAXC>
 __global__ void __launch_bounds__(kSalThreads)
 saliency_rows(const T* __restrict__ x, const T* __restrict__ xref, const float* __restrict__ fw,
               int L, int N, int D, double xi, float* __restrict__ s_out,
@@ -32,23 +35,40 @@ saliency_rows(const T* __restrict__ x, const T* __restrict__ xref, const float* 
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * (kSalThreads / kWave) + wave;
   if (row >= L) return;
-  constexpr int V = Elem<T>::kPerVec;
   const T* xr = x + row * D;
   const T* rr = xref + row * D;
-  const int nvec = D / V;
+  const int nch = D / 8;
   double num = 0.0, den = 0.0;
-#pragma unroll 4
-  for (int c = lane; c < nvec; c += kWave) {
-    const uint4 a = ldg16(xr + static_cast<int64_t>(c) * V);
-    const uint4 b = ldg16(rr + static_cast<int64_t>(c) * V);
-    float fa[V], fb[V];
-    unpack16(a, fa, static_cast<const T*>(nullptr));
-    unpack16(b, fb, static_cast<const T*>(nullptr));
+  auto add8 = [&](const Raw8<T>& a, const Raw8<T>& b) __attribute__((always_inline)) {
+    float fa[8], fb[8];
+    a.unpack(fa);
+    b.unpack(fb);
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
+    for (int j = 0; j < 8; ++j) {
       const double da = fa[j], db = fb[j];
       num += fabs(da - db);
       den += fabs(db);
+    }
+  };
+  if (MAXC > 0) {
+    constexpr int R = MAXC > 0 ? MAXC : 1;
+    Raw8<T> ra[R], rb[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int c = lane + u * kWave;
+      const int cc = c < nch ? c : nch - 1;  // past the row end: in-bounds re-load, not added
+      ra[u].load(xr + cc * 8);
+      rb[u].load(rr + cc * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < R; ++u)
+      if (lane + u * kWave < nch) add8(ra[u], rb[u]);
+  } else {
+    for (int c = lane; c < nch; c += kWave) {
+      Raw8<T> a, b;
+      a.load(xr + c * 8);
+      b.load(rr + c * 8);
+      add8(a, b);
     }
   }
   num = wave_sum(num);
@@ -70,6 +90,10 @@ __device__ __forceinline__ uint32_t rank_key(float s) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// R > 0: the L keys are loaded once into registers (key r*1024 + tid in
+// slot r, L <= 1024 R), all loads in flight together; every later pass works
+// on the registers.  R == 0: keys are re-read from s on every pass (any L).
+template <int R>
 __global__ void __launch_bounds__(kSelThreads)
 select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float threshold,
             const double* __restrict__ num, const double* __restrict__ den, double xi,
@@ -81,6 +105,23 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
   __shared__ double red_n[kSelWaves], red_d[kSelWaves];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const uint64_t lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+
+  constexpr int RR = R > 0 ? R : 1;
+  uint32_t kr[RR];
+  if constexpr (R > 0) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int i = r * kSelThreads + tid;
+      kr[r] = i < L ? rank_key(s[i]) : 0u;
+    }
+  }
+  const int nr = R > 0 ? R : (L + kSelThreads - 1) / kSelThreads;
+  auto key_of = [&](int r, int i) __attribute__((always_inline)) -> uint32_t {
+    if constexpr (R > 0)
+      return kr[r];
+    else
+      return i < L ? rank_key(s[i]) : 0u;
+  };
 
   // (1) step-level relative change, fixed summation order
   if (step_delta != nullptr) {
@@ -124,9 +165,23 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
       const int shift = 24 - 8 * pass;
       for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
       __syncthreads();
-      for (int i = tid; i < L; i += kSelThreads) {
-        const uint32_t key = rank_key(s[i]);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 0xffu], 1u);
+#pragma unroll
+      for (int r = 0; r < (R > 0 ? R : 1); ++r) {
+        for (int rr = (R > 0 ? r : 0); rr < (R > 0 ? r + 1 : nr); ++rr) {
+          const int i = rr * kSelThreads + tid;
+          const uint32_t key = key_of(rr, i);
+          const bool in = i < L && (key & pmask) == prefix;
+          const uint32_t bin = (key >> shift) & 0xffu;
+          // the lanes that share the first active lane's bin add with one atomic
+          const uint64_t act = __ballot(in);
+          if (act != 0ull) {
+            const int leader = __ffsll(static_cast<long long>(act)) - 1;
+            const uint32_t lbin = static_cast<uint32_t>(__shfl(static_cast<int>(bin), leader));
+            const uint64_t same = __ballot(in && bin == lbin);
+            if (lane == leader) atomicAdd(&hist[lbin], static_cast<uint32_t>(__popcll(same)));
+            if (in && bin != lbin) atomicAdd(&hist[bin], 1u);
+          }
+        }
       }
       __syncthreads();
       if (wave == 0) {
@@ -174,40 +229,43 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
 
   // (3) stable compaction in index order
   uint32_t base_eq = 0, base_sel = 0;
-  for (int c0 = 0; c0 < L; c0 += kSelThreads) {
-    const int i = c0 + tid;
-    const bool valid = i < L;
-    const uint32_t key = valid ? rank_key(s[i]) : 0u;
-    const bool gt = valid && key > thr;
-    const bool eq = valid && take_eq && key == thr;
-    const uint64_t beq = __ballot(eq);
-    if (lane == 0) wcnt[0][wave] = static_cast<uint32_t>(__popcll(beq));
-    __syncthreads();
-    uint32_t eq_before = base_eq, eq_total = 0;
-    for (int w = 0; w < kSelWaves; ++w) {
-      const uint32_t v = wcnt[0][w];
-      if (w < wave) eq_before += v;
-      eq_total += v;
+#pragma unroll
+  for (int r = 0; r < (R > 0 ? R : 1); ++r) {
+    for (int rr = (R > 0 ? r : 0); rr < (R > 0 ? r + 1 : nr); ++rr) {
+      const int i = rr * kSelThreads + tid;
+      const bool valid = i < L;
+      const uint32_t key = key_of(rr, i);
+      const bool gt = valid && key > thr;
+      const bool eq = valid && take_eq && key == thr;
+      const uint64_t beq = __ballot(eq);
+      if (lane == 0) wcnt[0][wave] = static_cast<uint32_t>(__popcll(beq));
+      __syncthreads();
+      uint32_t eq_before = base_eq, eq_total = 0;
+      for (int w = 0; w < kSelWaves; ++w) {
+        const uint32_t v = wcnt[0][w];
+        if (w < wave) eq_before += v;
+        eq_total += v;
+      }
+      eq_before += static_cast<uint32_t>(__popcll(beq & lt_mask));
+      const bool sel = gt || (eq && eq_before < need_eq);
+      const uint64_t bsel = __ballot(sel);
+      if (lane == 0) wcnt[1][wave] = static_cast<uint32_t>(__popcll(bsel));
+      __syncthreads();
+      uint32_t pos = base_sel, sel_total = 0;
+      for (int w = 0; w < kSelWaves; ++w) {
+        const uint32_t v = wcnt[1][w];
+        if (w < wave) pos += v;
+        sel_total += v;
+      }
+      pos += static_cast<uint32_t>(__popcll(bsel & lt_mask));
+      if (valid) {
+        mask[i] = sel ? 1 : 0;
+        if (sel) idx[pos] = i;
+      }
+      base_eq += eq_total;
+      base_sel += sel_total;
+      __syncthreads();  // wcnt is rewritten by the next chunk
     }
-    eq_before += static_cast<uint32_t>(__popcll(beq & lt_mask));
-    const bool sel = gt || (eq && eq_before < need_eq);
-    const uint64_t bsel = __ballot(sel);
-    if (lane == 0) wcnt[1][wave] = static_cast<uint32_t>(__popcll(bsel));
-    __syncthreads();
-    uint32_t pos = base_sel, sel_total = 0;
-    for (int w = 0; w < kSelWaves; ++w) {
-      const uint32_t v = wcnt[1][w];
-      if (w < wave) pos += v;
-      sel_total += v;
-    }
-    pos += static_cast<uint32_t>(__popcll(bsel & lt_mask));
-    if (valid) {
-      mask[i] = sel ? 1 : 0;
-      if (sel) idx[pos] = i;
-    }
-    base_eq += eq_total;
-    base_sel += sel_total;
-    __syncthreads();  // wcnt is rewritten by the next chunk
   }
   if (tid == 0) *n_sel = static_cast<int32_t>(base_sel);
 }
@@ -217,17 +275,42 @@ hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const 
                          double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
                          double* step_delta, hipStream_t stream) {
   const dim3 grid((L + (kSalThreads / kWave) - 1) / (kSalThreads / kWave));
-  hipError_t e;
-  if (dtype_bf16)
-    e = ECHO_LAUNCH("saliency_rows_bf16", saliency_rows<bf16_t>, grid, dim3(kSalThreads), 0, stream,
-                    static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(xref), fw, L, N, D, xi,
-                    s, num, den);
-  else
-    e = ECHO_LAUNCH("saliency_rows_f32", saliency_rows<float>, grid, dim3(kSalThreads), 0, stream,
-                    static_cast<const float*>(x), static_cast<const float*>(xref), fw, L, N, D, xi,
-                    s, num, den);
+  const int per_lane = (D / 8 + kWave - 1) / kWave;
+  hipError_t e = hipErrorInvalidValue;
+  bool done = false;
+#define ECHO_SAL_CASE(MC)                                                                        \
+  if (!done && (MC == 0 || per_lane <= MC)) {                                                    \
+    done = true;                                                                                 \
+    if (dtype_bf16)                                                                              \
+      e = ECHO_LAUNCH("saliency_rows_bf16", (saliency_rows<bf16_t, MC>), grid, dim3(kSalThreads), \
+                      0, stream, static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(xref), \
+                      fw, L, N, D, xi, s, num, den);                                             \
+    else                                                                                         \
+      e = ECHO_LAUNCH("saliency_rows_f32", (saliency_rows<float, MC>), grid, dim3(kSalThreads),   \
+                      0, stream, static_cast<const float*>(x), static_cast<const float*>(xref),   \
+                      fw, L, N, D, xi, s, num, den);                                             \
+  }
+  ECHO_SAL_CASE(1)
+  ECHO_SAL_CASE(2)
+  ECHO_SAL_CASE(3)
+  ECHO_SAL_CASE(4)
+  ECHO_SAL_CASE(6)
+  ECHO_SAL_CASE(8)
+  ECHO_SAL_CASE(10)
+  ECHO_SAL_CASE(12)
+  ECHO_SAL_CASE(16)
+  ECHO_SAL_CASE(0)
+#undef ECHO_SAL_CASE
   if (e != hipSuccess) return e;
-  return ECHO_LAUNCH("select_rows", select_rows, dim3(1), dim3(kSelThreads), 0, stream, s, L, k,
+#define ECHO_SEL_CASE(RK)                                                                     \
+  if (L <= RK * kSelThreads)                                                                  \
+    return ECHO_LAUNCH("select_rows", select_rows<RK>, dim3(1), dim3(kSelThreads), 0, stream, s, \
+                       L, k, threshold_mode, threshold, num, den, xi, idx, mask, n_sel, step_delta);
+  ECHO_SEL_CASE(8)
+  ECHO_SEL_CASE(32)
+  ECHO_SEL_CASE(80)
+#undef ECHO_SEL_CASE
+  return ECHO_LAUNCH("select_rows", select_rows<0>, dim3(1), dim3(kSelThreads), 0, stream, s, L, k,
                      threshold_mode, threshold, num, den, xi, idx, mask, n_sel, step_delta);
 }
 

@@ -129,6 +129,15 @@ def test_select_720p_shape():
     _select_case(w, [w.K])
 
 
+@pytest.mark.parametrize("grid", [(64, 64), (60, 64)], ids=["81920tok", "96000tok"])
+def test_select_register_limit(grid):
+    # 81920 keys is the most the register-resident selection holds (80 per
+    # thread); 96000 takes the variant that re-reads the keys on every pass
+    w = synth.TINY.with_(name=f"select_{grid[0]}x{grid[1]}", T=20 if grid == (64, 64) else 25,
+                         grid=grid, ratio=0.3)
+    _select_case(w, [1, w.K, w.L - 1, w.L])
+
+
 # -------------------------------------------------------------------- cache
 
 @pytest.mark.parametrize("w", [synth.TINY, RAGGED, synth.SMALL, synth.WAN14B_480P],
