@@ -147,7 +147,16 @@ int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref,
  * L*D, F*D, n_sel*F each below 2^30 elements (bf16 MFMA path; other shapes
  * return ECHO_EUNSUPPORTED); ECHO_F32 with D % 4 == 0, (D/H) % 4 == 0, D/H <= 128,
  * F % 4 == 0 (fp32 path for small shapes).  D <= 16384, F <= 65536.
+ * Without ECHO_BLOCK_BATCH_INVARIANT the bf16 path splits the attention work
+ * that does not fill a last round of the device along the keys (merged in
+ * fp32), so a row's rounding may depend on how many rows are selected; the
+ * result stays within the same tolerance of the definition either way.
  */
+/* echo_block_cfg.flags */
+#define ECHO_BLOCK_BATCH_INVARIANT 1 /* every token's y_sel row is bit-identical for
+                                        any idx that contains the token (no work is
+                                        split across workgroups by problem size) */
+
 typedef struct {
   int32_t L;
   int32_t D;
@@ -155,6 +164,7 @@ typedef struct {
   int32_t F;
   int32_t dtype;
   float ln_eps;
+  int32_t flags;      /* 0 or ECHO_BLOCK_BATCH_INVARIANT; other bits: ECHO_EINVAL */
 } echo_block_cfg;
 
 typedef struct {

@@ -15,6 +15,7 @@ HEADER = os.path.join(HERE, "..", "include", "echo.h")
 
 ECHO_OK, ECHO_EINVAL, ECHO_EUNSUPPORTED, ECHO_EWORKSPACE, ECHO_EDEVICE = range(5)
 ECHO_F32, ECHO_BF16 = 0, 1
+ECHO_BLOCK_BATCH_INVARIANT = 1
 
 c_int32, c_int64, c_size_t, c_void_p, c_float, c_double = (
     ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float,
@@ -33,7 +34,7 @@ class SelectCfg(ctypes.Structure):
 
 class BlockCfg(ctypes.Structure):
     _fields_ = [("L", c_int32), ("D", c_int32), ("H", c_int32), ("F", c_int32),
-                ("dtype", c_int32), ("ln_eps", c_float)]
+                ("dtype", c_int32), ("ln_eps", c_float), ("flags", c_int32)]
 
 
 class BlockWeights(ctypes.Structure):

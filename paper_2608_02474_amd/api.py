@@ -173,8 +173,10 @@ def block_weights(params: dict) -> BlockWeights:
 
 def block_partial(params: dict, x: torch.Tensor, idx: torch.Tensor, n_sel: int, H: int,
                   ln_eps: float = 1e-6, y_sel: torch.Tensor | None = None,
-                  workspace: Workspace | None = None, _weights: BlockWeights | None = None):
-    """y_sel [n_sel, D] fp32 = block output of tokens idx[:n_sel]."""
+                  workspace: Workspace | None = None, _weights: BlockWeights | None = None,
+                  batch_invariant: bool = False):
+    """y_sel [n_sel, D] fp32 = block output of tokens idx[:n_sel].  With
+    batch_invariant, each row is bit-identical for any selection containing it."""
     lib = _lib_handle()
     _dev(x, "x")
     _dev(idx, "idx", torch.int32)
@@ -184,7 +186,8 @@ def block_partial(params: dict, x: torch.Tensor, idx: torch.Tensor, n_sel: int, 
         if params[n].dtype != x.dtype:
             raise TypeError(f"{n} must have the activation dtype {x.dtype}")
     _dev(params["mod"], "mod", torch.float32)
-    cfg = BlockCfg(L, D, H, F, _echo_dtype(x), float(ln_eps))
+    cfg = BlockCfg(L, D, H, F, _echo_dtype(x), float(ln_eps),
+                   _lib.ECHO_BLOCK_BATCH_INVARIANT if batch_invariant else 0)
     w = _weights if _weights is not None else block_weights(params)
     if y_sel is None:
         y_sel = torch.empty((max(n_sel, 1), D), dtype=torch.float32, device=x.device)

@@ -90,7 +90,8 @@ template <int QB, int WAVES>
 __global__ void __launch_bounds__(WAVES * 64, 1)
 attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k,
               const bf16_t* __restrict__ v, int64_t ldkv, int Mq, int L, int H, float scale_log2,
-              bf16_t* __restrict__ out, int64_t ldo) {
+              bf16_t* __restrict__ out, int64_t ldo, int item_base, int nsplit, int kt_per_split,
+              float* __restrict__ part_o, float* __restrict__ part_ml) {
   typedef AttCfg<QB, WAVES> C;
   constexpr int ATT_NSTAGE = C::kStages;
   constexpr int NLD = 16 / WAVES;  // 1 KB direct-load instructions per wave per K (or V) tile
@@ -101,14 +102,26 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   const int wave = tid / kWave, lane = tid % kWave, l32 = lane & 31, hi = lane >> 5;
   const int g16 = lane >> 4, i16 = lane & 15;
 
+  // Work item = (head, query tile).  Unsplit launches (nsplit == 1) take the
+  // items [item_base, item_base + gridDim.x), remapped so that each XCD works
+  // through a contiguous range; split launches give workgroup g the key-tile
+  // range split g % nsplit of item item_base + g / nsplit and leave partial
+  // results for attn_combine.
   const int ntq = (Mq + C::kQ - 1) / C::kQ;
-  const int total = ntq * H;
-  int pid = blockIdx.x;
-  {
+  const int nkt_all = (L + ATT_KT - 1) / ATT_KT;
+  int item, split = 0;
+  if (nsplit == 1) {
+    const int total = gridDim.x;
+    const int pid = blockIdx.x;
     const int qq = total / 8, r = total % 8, xcd = pid % 8, loc = pid / 8;
-    pid = xcd * qq + (xcd < r ? xcd : r) + loc;
+    item = item_base + xcd * qq + (xcd < r ? xcd : r) + loc;
+  } else {
+    item = item_base + blockIdx.x / nsplit;
+    split = blockIdx.x % nsplit;
   }
-  const int head = pid / ntq, qt = pid % ntq;
+  const int head = item / ntq, qt = item % ntq;
+  const int t_begin = split * kt_per_split;  // first key tile of this workgroup
+  const int nkt = (nkt_all - t_begin < kt_per_split ? nkt_all - t_begin : kt_per_split);  // >= 1
   const int64_t hoff = static_cast<int64_t>(head) * ATT_DH;
 
   // ---- query fragments: block b, lane holds q[row][16 s + 8 hi .. +7] for the 8 k16-steps
@@ -334,9 +347,9 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     pv(stage_c, pf);
   };
 
-  const int nkt = (L + ATT_KT - 1) / ATT_KT;
-  issue_tile(0, 0);
-  if (nkt > 1) issue_tile(1, 1);
+  // tiles are counted from t_begin below: t is relative, t_begin + t absolute
+  issue_tile(t_begin, 0);
+  if (nkt > 1) issue_tile(t_begin + 1, 1);
 
   {
     // iteration t: tile t sits in stage t%3, tile t+1 is in flight
@@ -350,9 +363,9 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       else
         __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      if (t + 2 < nkt) issue_tile(t + 2, ST2);
+      if (t + 2 < nkt) issue_tile(t_begin + t + 2, ST2);
       compute_s(std::integral_constant<int, ST>{}, sacc);
-      softmax_pv(std::integral_constant<int, ST>{}, sacc, t * ATT_KT);
+      softmax_pv(std::integral_constant<int, ST>{}, sacc, (t_begin + t) * ATT_KT);
     };
     for (int t = 0; t < nkt; t += 3) {
       iteration(std::integral_constant<int, 0>{}, t);
@@ -361,6 +374,28 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       if (t + 2 >= nkt) break;
       iteration(std::integral_constant<int, 2>{}, t + 2);
     }
+  }
+
+  if (part_o != nullptr) {
+    // split workgroup: unnormalised output in the accumulator layout (for each
+    // (b, d, r) the 64 lanes write 256 contiguous bytes), running reference
+    // maximum and row sum per query
+    const int64_t unit = blockIdx.x;
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const float lsum = pair_sum(l_run[b]);
+      const int qloc = (wave * QB + b) * 32 + l32;
+      if (hi == 0) {
+        part_ml[(unit * C::kQ + qloc) * 2] = m_run[b];
+        part_ml[(unit * C::kQ + qloc) * 2 + 1] = lsum;
+      }
+      float* po = part_o + ((unit * WAVES + wave) * QB + b) * (4 * 16 * kWave);
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) po[(d * 16 + r) * kWave + lane] = o[b][d][r];
+    }
+    return;
   }
 
   // normalise and write through LDS so that global stores are full 16-byte rows
@@ -390,22 +425,113 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
 }
 
+// Merge the key-range splits of the tail items: o = sum_s 2^{(m_s - m) c} o_s
+// / sum_s 2^{(m_s - m) c} l_s with m = max_s m_s (c = scale * log2 e).  One
+// thread per (item, query, dh) output element, splits added in order.
+template <int QB, int WAVES>
+__global__ void __launch_bounds__(256)
+attn_combine(const float* __restrict__ part_o, const float* __restrict__ part_ml, int nitems,
+             int nsplit, int item_base, int Mq, int H, float scale_log2, bf16_t* __restrict__ out,
+             int64_t ldo) {
+  typedef AttCfg<QB, WAVES> C;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<int64_t>(nitems) * C::kQ * ATT_DH) return;
+  const int dh = static_cast<int>(e % ATT_DH);
+  const int qloc = static_cast<int>((e / ATT_DH) % C::kQ);
+  const int j = static_cast<int>(e / (static_cast<int64_t>(ATT_DH) * C::kQ));
+  const int ntq = (Mq + C::kQ - 1) / C::kQ;
+  const int item = item_base + j, head = item / ntq, qt = item % ntq;
+  const int qg = qt * C::kQ + qloc;
+  if (qg >= Mq) return;
+  // accumulator coordinates of (qloc, dh)
+  const int wave = qloc / (QB * 32), b = (qloc / 32) % QB, l32 = qloc % 32;
+  const int d = dh / 32, rem = dh % 32;
+  const int hi = (rem >> 2) & 1, r = 4 * (rem >> 3) + (rem & 3);
+  const int lane = l32 + 32 * hi;
+  float m = -INFINITY;
+  for (int sp = 0; sp < nsplit; ++sp) {
+    const int64_t unit = static_cast<int64_t>(j) * nsplit + sp;
+    m = fmaxf(m, part_ml[(unit * C::kQ + qloc) * 2]);
+  }
+  float lsum = 0.0f, acc = 0.0f;
+  for (int sp = 0; sp < nsplit; ++sp) {
+    const int64_t unit = static_cast<int64_t>(j) * nsplit + sp;
+    const float w = __builtin_amdgcn_exp2f((part_ml[(unit * C::kQ + qloc) * 2] - m) * scale_log2);
+    lsum += w * part_ml[(unit * C::kQ + qloc) * 2 + 1];
+    acc += w * part_o[((unit * WAVES + wave) * QB + b) * (4 * 16 * kWave) + (d * 16 + r) * kWave + lane];
+  }
+  out[static_cast<int64_t>(qg) * ldo + static_cast<int64_t>(head) * ATT_DH + dh] = f32_to_bf16(acc / lsum);
+}
+
+int attn_cu_count() {
+  static int n = [] {
+    int dev = 0, cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0)
+      cu = 256;
+    return cu;
+  }();
+  return n;
+}
+
+// Work items beyond the last full round of one workgroup per CU (the kernel's
+// LDS allows one) would leave most CUs idle for a whole round; they are split
+// along the keys into nsplit parts that fill that round together and merged by
+// attn_combine.  The three launches are timed as one attention call.
 template <int QB, int WAVES>
 hipError_t launch_attn_variant(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                                int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
-                               hipStream_t stream) {
+                               float* part, size_t part_bytes, hipStream_t stream) {
   if (Mq <= 0) return hipSuccess;
   typedef AttCfg<QB, WAVES> C;
   const float scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(ATT_DH)));
   const int ntq = (Mq + C::kQ - 1) / C::kQ;
-  return ECHO_LAUNCH("attn_fwd_bf16", (attn_fwd_bf16<QB, WAVES>), dim3(ntq * H), dim3(C::kThreads), 0,
-                     stream, q, ldq, k, v, ldkv, Mq, L, H, scale_log2, out, ldo);
+  const int total = ntq * H;
+  const int nkt = (L + ATT_KT - 1) / ATT_KT;
+  const int ncu = attn_cu_count();
+  const int tail = total % ncu;
+  int nsplit = tail > 0 ? ncu / tail : 1;
+  nsplit = nsplit < nkt ? nsplit : nkt;
+  const size_t unit_bytes = sizeof(float) * C::kQ * (ATT_DH + 2);
+  while (nsplit > 1 && static_cast<size_t>(tail) * nsplit * unit_bytes > part_bytes) --nsplit;
+  if (part == nullptr) nsplit = 1;
+  ::echo::TimedLaunch scope("attn_fwd_bf16", stream);
+  if (nsplit < 2) {
+    hipLaunchKernelGGL((attn_fwd_bf16<QB, WAVES>), dim3(total), dim3(C::kThreads), 0, stream, q, ldq, k, v,
+                       ldkv, Mq, L, H, scale_log2, out, ldo, 0, 1, nkt, nullptr, nullptr);
+    return hipGetLastError();
+  }
+  const int kps = (nkt + nsplit - 1) / nsplit;  // key tiles per split
+  nsplit = (nkt + kps - 1) / kps;               // every split non-empty
+  const int full = total - tail;
+  if (full > 0) {
+    hipLaunchKernelGGL((attn_fwd_bf16<QB, WAVES>), dim3(full), dim3(C::kThreads), 0, stream, q, ldq, k, v,
+                       ldkv, Mq, L, H, scale_log2, out, ldo, 0, 1, nkt, nullptr, nullptr);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  float* part_o = part;
+  float* part_ml = part + static_cast<size_t>(tail) * nsplit * C::kQ * ATT_DH;
+  hipLaunchKernelGGL((attn_fwd_bf16<QB, WAVES>), dim3(tail * nsplit), dim3(C::kThreads), 0, stream, q, ldq, k,
+                     v, ldkv, Mq, L, H, scale_log2, out, ldo, full, nsplit, kps, part_o, part_ml);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t elems = static_cast<int64_t>(tail) * C::kQ * ATT_DH;
+  hipLaunchKernelGGL((attn_combine<QB, WAVES>), dim3(static_cast<unsigned>((elems + 255) / 256)), dim3(256), 0,
+                     stream, part_o, part_ml, tail, nsplit, full, Mq, H, scale_log2, out, ldo);
+  return hipGetLastError();
+}
+
+size_t attn_partial_bytes() {
+  // 256 units (one per CU of a 256-CU device) of 256 queries x (128 outputs +
+  // maximum + sum) floats; on a larger device the tail is split less
+  return sizeof(float) * 256 * 256 * (ATT_DH + 2);
 }
 
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
-                            hipStream_t stream) {
-  return launch_attn_variant<1, 8>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, stream);
+                            float* part, size_t part_bytes, hipStream_t stream) {
+  return launch_attn_variant<1, 8>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, part, part_bytes, stream);
 }
 
 }  // namespace echo

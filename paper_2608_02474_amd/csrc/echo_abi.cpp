@@ -103,7 +103,7 @@ size_t select_ws(const echo_select_cfg* c) {
 bool block_cfg_ok(const echo_block_cfg* c) {
   return c != nullptr && c->L >= 1 && c->D >= 8 && c->H >= 1 && c->F >= 8 && ok_dtype(c->dtype) &&
          c->D <= 16384 && c->F <= 65536 && (c->D % c->H) == 0 && (c->D % 8) == 0 &&
-         (c->F % 8) == 0 && c->ln_eps >= 0.0f;
+         (c->F % 8) == 0 && c->ln_eps >= 0.0f && (c->flags & ~ECHO_BLOCK_BATCH_INVARIANT) == 0;
 }
 bool block_supported(const echo_block_cfg* c) {
   const int dh = c->D / c->H;
@@ -116,6 +116,7 @@ bool block_supported(const echo_block_cfg* c) {
 struct BlockWs {
   void *a, *kv, *q, *o, *b, *h;
   float* x1;
+  float* part;  // bf16 path: partial results of the key-split attention tail
   size_t bytes;
 };
 BlockWs block_ws_layout(const echo_block_cfg* c, int64_t n, char* base) {
@@ -135,6 +136,7 @@ BlockWs block_ws_layout(const echo_block_cfg* c, int64_t n, char* base) {
   w.x1 = reinterpret_cast<float*>(take(m * D * 4));
   w.b = take(m * D * es);
   w.h = take(m * F * es);
+  if (c->dtype == ECHO_BF16) w.part = reinterpret_cast<float*>(take(attn_partial_bytes()));
   w.bytes = off;
   return w;
 }
@@ -253,7 +255,10 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
     if ((e = launch_gemm_bf16("gemm_kv_bf16", 0, g, st)) != hipSuccess) return device_status(e);
     const bf16_t* kvp = static_cast<const bf16_t*>(ws.kv);
     if ((e = launch_attn_bf16(static_cast<P>(ws.q), D, kvp, kvp + D, 2 * D, n, L, H,
-                              static_cast<bf16_t*>(ws.o), D, st)) != hipSuccess)
+                              static_cast<bf16_t*>(ws.o), D,
+                              (cfg->flags & ECHO_BLOCK_BATCH_INVARIANT) ? nullptr : ws.part,
+                              attn_partial_bytes(), st)) !=
+        hipSuccess)
       return device_status(e);
     // x1 = x[idx] + gate1 * (o Wo^T + bo)
     g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, n, static_cast<P>(w->wo), static_cast<P>(w->wo), D,

@@ -74,9 +74,12 @@ hipError_t launch_modln_x1(int dtype_bf16, const float* x1, int M, int D, const 
 hipError_t launch_gemm_bf16(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream);
 hipError_t launch_gemm_f32(const char* name, int epi, const GemmF32Args& a, hipStream_t stream);
 
+// `part` (part_bytes, attn_partial_bytes() is enough) holds the partial
+// results of the key-split tail work items; with part == nullptr nothing is split.
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
-                            hipStream_t stream);
+                            float* part, size_t part_bytes, hipStream_t stream);
+size_t attn_partial_bytes();
 hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, const float* v, int64_t ldkv,
                            int Mq, int L, int H, int dh, float* out, int64_t ldo, hipStream_t stream);
 

@@ -89,6 +89,7 @@ def test_block_rejects_before_launch(lib):
     bad = _lib.BlockWeights(*([0x20000] * 12 + [0x20008]))                            # misaligned mod
     assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6), weights=bad) == _lib.ECHO_EINVAL
     # n_sel == 0 is a successful no-op that launches nothing
+    assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6, 2)) == _lib.ECHO_EINVAL      # unknown flag
     assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6), n=0) == _lib.ECHO_OK
 
 
