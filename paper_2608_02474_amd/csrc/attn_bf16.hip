@@ -463,17 +463,6 @@ attn_combine(const float* __restrict__ part_o, const float* __restrict__ part_ml
   out[static_cast<int64_t>(qg) * ldo + static_cast<int64_t>(head) * ATT_DH + dh] = f32_to_bf16(acc / lsum);
 }
 
-int attn_cu_count() {
-  static int n = [] {
-    int dev = 0, cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0)
-      cu = 256;
-    return cu;
-  }();
-  return n;
-}
-
 // Work items beyond the last full round of one workgroup per CU (the kernel's
 // LDS allows one) would leave most CUs idle for a whole round; they are split
 // along the keys into nsplit parts that fill that round together and merged by
@@ -488,7 +477,7 @@ hipError_t launch_attn_variant(const bf16_t* q, int64_t ldq, const bf16_t* k, co
   const int ntq = (Mq + C::kQ - 1) / C::kQ;
   const int total = ntq * H;
   const int nkt = (L + ATT_KT - 1) / ATT_KT;
-  const int ncu = attn_cu_count();
+  const int ncu = device_cu_count();
   const int tail = total % ncu;
   int nsplit = tail > 0 ? ncu / tail : 1;
   nsplit = nsplit < nkt ? nsplit : nkt;

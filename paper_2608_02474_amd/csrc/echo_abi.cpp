@@ -53,6 +53,23 @@ TimedLaunch::~TimedLaunch() {
   if (slot >= 0) (void)hipEventRecord(g_records[slot].stop, stream);
 }
 
+int device_cu_count() {
+  static const int n = [] {
+    int dev = 0, cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0)
+      cu = 256;
+    return cu;
+  }();
+  return n;
+}
+
+size_t block_partial_bytes() {
+  const size_t gemm = sizeof(float) * 256 * 256 * 256;  // 256 fp32 tiles of 256 x 256
+  const size_t attn = attn_partial_bytes();
+  return gemm > attn ? gemm : attn;
+}
+
 }  // namespace echo
 
 using namespace echo;
@@ -136,7 +153,7 @@ BlockWs block_ws_layout(const echo_block_cfg* c, int64_t n, char* base) {
   w.x1 = reinterpret_cast<float*>(take(m * D * 4));
   w.b = take(m * D * es);
   w.h = take(m * F * es);
-  if (c->dtype == ECHO_BF16) w.part = reinterpret_cast<float*>(take(attn_partial_bytes()));
+  if (c->dtype == ECHO_BF16) w.part = reinterpret_cast<float*>(take(block_partial_bytes()));
   w.bytes = off;
   return w;
 }
@@ -243,28 +260,34 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
   if (bf) {
     typedef const bf16_t* P;
     GemmBf16Args g{};
+    // partial results of the split tails (none when every row must be batch-invariant)
+    float* part = (cfg->flags & ECHO_BLOCK_BATCH_INVARIANT) ? nullptr : ws.part;
+    auto with_part = [&](GemmBf16Args a) {
+      a.part = part;
+      a.part_bytes = block_partial_bytes();
+      return a;
+    };
     // q = a[idx] Wq^T + bq
     g = GemmBf16Args{static_cast<P>(ws.a), D, idx, L, static_cast<P>(w->wq), static_cast<P>(w->wq), D, D,
                      static_cast<P>(w->bq), static_cast<P>(w->bq), n, D, D, ws.q, D,
                      nullptr, nullptr, 0, nullptr, 0};
-    if ((e = launch_gemm_bf16("gemm_q_bf16", 0, g, st)) != hipSuccess) return device_status(e);
+    if ((e = launch_gemm_bf16("gemm_q_bf16", 0, with_part(g), st)) != hipSuccess) return device_status(e);
     // [k | v] = a [Wk; Wv]^T + [bk; bv], one N = 2D GEMM over all L rows
     g = GemmBf16Args{static_cast<P>(ws.a), D, nullptr, L, static_cast<P>(w->wk), static_cast<P>(w->wv), D,
                      D, static_cast<P>(w->bk), static_cast<P>(w->bv), L, 2 * D, D, ws.kv, 2 * D,
                      nullptr, nullptr, 0, nullptr, 0};
-    if ((e = launch_gemm_bf16("gemm_kv_bf16", 0, g, st)) != hipSuccess) return device_status(e);
+    if ((e = launch_gemm_bf16("gemm_kv_bf16", 0, with_part(g), st)) != hipSuccess) return device_status(e);
     const bf16_t* kvp = static_cast<const bf16_t*>(ws.kv);
     if ((e = launch_attn_bf16(static_cast<P>(ws.q), D, kvp, kvp + D, 2 * D, n, L, H,
                               static_cast<bf16_t*>(ws.o), D,
-                              (cfg->flags & ECHO_BLOCK_BATCH_INVARIANT) ? nullptr : ws.part,
-                              attn_partial_bytes(), st)) !=
+                              part, block_partial_bytes(), st)) !=
         hipSuccess)
       return device_status(e);
     // x1 = x[idx] + gate1 * (o Wo^T + bo)
     g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, n, static_cast<P>(w->wo), static_cast<P>(w->wo), D,
                      D, static_cast<P>(w->bo), static_cast<P>(w->bo), n, D, D, ws.x1, D,
                      mod + 2 * D, x, D, idx, 1};
-    if ((e = launch_gemm_bf16("gemm_o_bf16", 2, g, st)) != hipSuccess) return device_status(e);
+    if ((e = launch_gemm_bf16("gemm_o_bf16", 2, with_part(g), st)) != hipSuccess) return device_status(e);
     if ((e = launch_modln_x1(1, ws.x1, n, D, mod + 3 * D, mod + 4 * D, cfg->ln_eps, ws.b, st)) !=
         hipSuccess)
       return device_status(e);
@@ -272,12 +295,12 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
     g = GemmBf16Args{static_cast<P>(ws.b), D, nullptr, n, static_cast<P>(w->w1), static_cast<P>(w->w1), F,
                      D, static_cast<P>(w->b1), static_cast<P>(w->b1), n, F, D, ws.h, F,
                      nullptr, nullptr, 0, nullptr, 0};
-    if ((e = launch_gemm_bf16("gemm_ffn_up_bf16", 1, g, st)) != hipSuccess) return device_status(e);
+    if ((e = launch_gemm_bf16("gemm_ffn_up_bf16", 1, with_part(g), st)) != hipSuccess) return device_status(e);
     // y_sel = x1 + gate2 * (h W2^T + b2)
     g = GemmBf16Args{static_cast<P>(ws.h), F, nullptr, n, static_cast<P>(w->w2), static_cast<P>(w->w2), D,
                      F, static_cast<P>(w->b2), static_cast<P>(w->b2), n, D, F, y_sel, D,
                      mod + 5 * D, ws.x1, D, nullptr, 0};
-    if ((e = launch_gemm_bf16("gemm_ffn_down_bf16", 2, g, st)) != hipSuccess) return device_status(e);
+    if ((e = launch_gemm_bf16("gemm_ffn_down_bf16", 2, with_part(g), st)) != hipSuccess) return device_status(e);
     return ECHO_OK;
   }
   typedef const float* P;

@@ -57,6 +57,70 @@ __device__ __forceinline__ float gelu_tanh_fast(float z) {
   return z / (1.0f + __expf(-2.0f * u));
 }
 
+// Grouped tile order: 8 tile-rows at a time, down the rows first, so that
+// consecutive tiles share B panels and a run of them shares A panels in L2.
+__host__ __device__ __forceinline__ void gemm_tile_of(int pid, int tm, int tn, int& tile_m, int& tile_n) {
+  constexpr int GROUP = 8;
+  const int group_size = GROUP * tn;
+  const int first_m = (pid / group_size) * GROUP;
+  const int gm = (tm - first_m) < GROUP ? (tm - first_m) : GROUP;
+  tile_m = first_m + (pid % group_size) % gm;
+  tile_n = (pid % group_size) / gm;
+}
+
+// Bias (and gate) of the 4 consecutive output columns col .. col+3.
+template <int EPI>
+__device__ __forceinline__ void gemm_col4(const GemmBf16Args& p, int col, float* bias, float* gate) {
+  const bf16_t* bias_p = col < p.n_split ? p.bias0 + col : p.bias1 + (col - p.n_split);
+  const uint2 bb = *reinterpret_cast<const uint2*>(bias_p);
+  bias[0] = __uint_as_float(bb.x << 16);
+  bias[1] = __uint_as_float(bb.x & 0xffff0000u);
+  bias[2] = __uint_as_float(bb.y << 16);
+  bias[3] = __uint_as_float(bb.y & 0xffff0000u);
+  if (EPI == EPI_GATE_RES) {
+    const float4 g = *reinterpret_cast<const float4*>(p.gate + col);
+    gate[0] = g.x; gate[1] = g.y; gate[2] = g.z; gate[3] = g.w;
+  }
+}
+
+// Output of 4 consecutive columns col .. col+3 of row `row` (acc4 = sums
+// without bias): bias, then GELU (bf16 out), plain (bf16 out) or residual +
+// gate * v (fp32 out).
+template <int EPI>
+__device__ __forceinline__ void gemm_store4(const GemmBf16Args& p, int row, int col, const float* acc4,
+                                            const float* bias, const float* gate) {
+  float v[4] = {acc4[0] + bias[0], acc4[1] + bias[1], acc4[2] + bias[2], acc4[3] + bias[3]};
+  if (EPI == EPI_GATE_RES) {
+    const int64_t rr = p.res_rows ? p.res_rows[row] : row;
+    float res[4];
+    if (p.res_bf16) {
+      const uint2 rb = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
+      res[0] = __uint_as_float(rb.x << 16);
+      res[1] = __uint_as_float(rb.x & 0xffff0000u);
+      res[2] = __uint_as_float(rb.y << 16);
+      res[3] = __uint_as_float(rb.y & 0xffff0000u);
+    } else {
+      const float4 rf = *reinterpret_cast<const float4*>(static_cast<const float*>(p.res) + rr * p.ldr + col);
+      res[0] = rf.x; res[1] = rf.y; res[2] = rf.z; res[3] = rf.w;
+    }
+    float4 o;
+    o.x = res[0] + gate[0] * v[0];
+    o.y = res[1] + gate[1] * v[1];
+    o.z = res[2] + gate[2] * v[2];
+    o.w = res[3] + gate[3] * v[3];
+    *reinterpret_cast<float4*>(static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
+  } else {
+    if (EPI == EPI_GELU) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_fast(v[e]);
+    }
+    uint2 o;
+    o.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+    o.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+    *reinterpret_cast<uint2*>(static_cast<bf16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
+  }
+}
+
 template <int BM, int BN, int WM, int WN, int NS, int BK>
 struct GemmCfg {
   static constexpr int kWaves = WM * WN;
@@ -82,19 +146,23 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
   const int wave = tid / kWave, lane = tid % kWave, l32 = lane & 31, hi = lane >> 5;
   const int wm = wave / WN, wn = wave % WN;
 
-  // ---- tile id: XCD-contiguous runs, then groups of 8 tile-rows
-  const int tm = (p.M + BM - 1) / BM, tn = p.N / BN, tiles = tm * tn;
-  int pid = blockIdx.x;
-  {
-    const int q = tiles / 8, r = tiles % 8, xcd = pid % 8, loc = pid / 8;
-    pid = xcd * q + (xcd < r ? xcd : r) + loc;
+  // ---- tile id.  Unsplit launches take tiles [tile_base, tile_base +
+  // gridDim.x) of the grouped order, remapped so that each XCD works through a
+  // contiguous run; split launches give workgroup g k-range g % nsplit of tile
+  // tile_base + g / nsplit.
+  const int tm = (p.M + BM - 1) / BM, tn = p.N / BN;
+  const bool split_k = p.nsplit > 1;
+  int pid, ksplit = 0;
+  if (!split_k) {
+    const int total = gridDim.x, g = blockIdx.x;
+    const int q = total / 8, r = total % 8, xcd = g % 8, loc = g / 8;
+    pid = p.tile_base + xcd * q + (xcd < r ? xcd : r) + loc;
+  } else {
+    pid = p.tile_base + blockIdx.x / p.nsplit;
+    ksplit = blockIdx.x % p.nsplit;
   }
-  constexpr int GROUP = 8;
-  const int group_size = GROUP * tn;
-  const int first_m = (pid / group_size) * GROUP;
-  const int gm = (tm - first_m) < GROUP ? (tm - first_m) : GROUP;
-  const int tile_m = first_m + (pid % group_size) % gm;
-  const int tile_n = (pid % group_size) / gm;
+  int tile_m, tile_n;
+  gemm_tile_of(pid, tm, tn, tile_m, tile_n);
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
   // ---- copy plan: copy c of this wave fills kRowsPerCopy tile rows (1 KB) of
@@ -209,11 +277,22 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
   // k-step kt+1 refills with kt+NS) and waited until at most its copies of
   // the newest NS-2 k-steps are outstanding, so after it stage (kt+1) % NS is
   // complete and its first fragments are read under the remaining MFMAs.
-  const int nk = p.K / BK;
+  const int nk_all = p.K / BK;
+  const int kt0 = split_k ? ksplit * p.kps : 0;  // first k-step of this workgroup
+  const int nk = split_k ? (nk_all - kt0 < p.kps ? nk_all - kt0 : p.kps) : nk_all;  // >= 1
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
-    if (s < nk) issue(s, s);
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm((NS - 2) * C::kCopies));  // k-step 0 complete
+    if (s < nk) issue(kt0 + s, s);
+  // Waits allow the copies of the NS-2 k-steps issued after the one needed;
+  // a range of fewer than NS-1 k-steps issued fewer, so it drains them all.
+  const bool short_range = nk < NS - 1;
+  auto wait_next = [&]() __attribute__((always_inline)) {
+    if (short_range)
+      __builtin_amdgcn_s_waitcnt(0);
+    else
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((NS - 2) * C::kCopies));
+  };
+  wait_next();  // k-step 0 complete
   __syncthreads();
   load(I0{}, 0, 0);
   int stage = 0;
@@ -223,7 +302,7 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
     // k-step kt + NS - 1 goes to the stage read at kt - 1; past the end the
     // last k-step is fetched again (in bounds, never read) so that every
     // k-step issues the same copies and the wait below is uniform.
-    const int kf = kt + NS - 1 < nk ? kt + NS - 1 : nk - 1;
+    const int kf = kt0 + (kt + NS - 1 < nk ? kt + NS - 1 : nk - 1);
     fill_a = p.A + static_cast<int64_t>(kf) * BK;
     fill_b = b_base + static_cast<int64_t>(kf) * BK;
     fill_off = fill * C::kStageBytes;
@@ -236,7 +315,7 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
     __builtin_amdgcn_sched_barrier(0);
     mma(ILAST{}, I0{}, IH{}, std::integral_constant<int, KS - 1>{});
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((NS - 2) * C::kCopies));
+    wait_next();  // k-step kt+1 complete
     __syncthreads();
     if (kt + 1 < nk) load(I0{}, next, 0);
     mma(ILAST{}, IH{}, IM{}, std::integral_constant<int, KS>{});
@@ -261,19 +340,8 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
   float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EP_LD;
   const int c_l = (lane % LPR) * 4;                   // first of this lane's 4 columns
   const int col = n0 + wn * (BN / WN) + c_l;           // global column (4 | col)
-  const bf16_t* bias_p = col < p.n_split ? p.bias0 + col : p.bias1 + (col - p.n_split);
   float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  {
-    const uint2 bb = *reinterpret_cast<const uint2*>(bias_p);
-    bias[0] = __uint_as_float(bb.x << 16);
-    bias[1] = __uint_as_float(bb.x & 0xffff0000u);
-    bias[2] = __uint_as_float(bb.y << 16);
-    bias[3] = __uint_as_float(bb.y & 0xffff0000u);
-    if (EPI == EPI_GATE_RES) {
-      const float4 g = *reinterpret_cast<const float4*>(p.gate + col);
-      gate[0] = g.x; gate[1] = g.y; gate[2] = g.z; gate[3] = g.w;
-    }
-  }
+  if (!split_k) gemm_col4<EPI>(p, col, bias, gate);
 #pragma unroll
   for (int i = 0; i < C::kTM; ++i) {
 #pragma unroll
@@ -285,58 +353,97 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
 #pragma unroll
     for (int q = 0; q < 32 / RPI; ++q) {
       const int r_l = q * RPI + lane / LPR;
-      const int row = m0 + wm * (BM / WM) + i * 32 + r_l;
+      const int trow = wm * (BM / WM) + i * 32 + r_l;  // row within the tile
       const float4 a4 = *reinterpret_cast<const float4*>(ep + r_l * EP_LD + c_l);
-      float v[4] = {a4.x + bias[0], a4.y + bias[1], a4.z + bias[2], a4.w + bias[3]};
-      if (row < p.M) {
-        if (EPI == EPI_GATE_RES) {
-          const int64_t rr = p.res_rows ? p.res_rows[row] : row;
-          float res[4];
-          if (p.res_bf16) {
-            const uint2 rb = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
-            res[0] = __uint_as_float(rb.x << 16);
-            res[1] = __uint_as_float(rb.x & 0xffff0000u);
-            res[2] = __uint_as_float(rb.y << 16);
-            res[3] = __uint_as_float(rb.y & 0xffff0000u);
-          } else {
-            const float4 rf = *reinterpret_cast<const float4*>(static_cast<const float*>(p.res) + rr * p.ldr + col);
-            res[0] = rf.x; res[1] = rf.y; res[2] = rf.z; res[3] = rf.w;
-          }
-          float4 o;
-          o.x = res[0] + gate[0] * v[0];
-          o.y = res[1] + gate[1] * v[1];
-          o.z = res[2] + gate[2] * v[2];
-          o.w = res[3] + gate[3] * v[3];
-          *reinterpret_cast<float4*>(static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
-        } else {
-          if (EPI == EPI_GELU) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_fast(v[e]);
-          }
-          uint2 o;
-          o.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-          o.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
-        }
+      if (split_k) {
+        // raw partial sums of this k-range, tile-local [BM][BN] per workgroup
+        *reinterpret_cast<float4*>(p.part + static_cast<int64_t>(blockIdx.x) * BM * BN +
+                                   static_cast<int64_t>(trow) * BN + (col - n0)) = a4;
+      } else if (m0 + trow < p.M) {
+        const float v[4] = {a4.x, a4.y, a4.z, a4.w};
+        gemm_store4<EPI>(p, m0 + trow, col, v, bias, gate);
       }
     }
   }
 }
 
+// Sum the k-range partials of the split tail tiles in split order and apply
+// the epilogue.  One thread per 4 output columns.
+template <int BM, int BN, int EPI>
+__global__ void __launch_bounds__(256) gemm_splitk_reduce(GemmBf16Args p, int ntail) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<int64_t>(ntail) * BM * (BN / 4)) return;
+  const int c4 = static_cast<int>(e % (BN / 4)), trow = static_cast<int>((e / (BN / 4)) % BM);
+  const int j = static_cast<int>(e / (static_cast<int64_t>(BM) * (BN / 4)));
+  const int tm = (p.M + BM - 1) / BM, tn = p.N / BN;
+  int tile_m, tile_n;
+  gemm_tile_of(p.tile_base + j, tm, tn, tile_m, tile_n);
+  const int row = tile_m * BM + trow;
+  if (row >= p.M) return;
+  float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int sp = 0; sp < p.nsplit; ++sp) {
+    const float4 a4 = *reinterpret_cast<const float4*>(
+        p.part + (static_cast<int64_t>(j) * p.nsplit + sp) * BM * BN + static_cast<int64_t>(trow) * BN + 4 * c4);
+    v[0] += a4.x;
+    v[1] += a4.y;
+    v[2] += a4.z;
+    v[3] += a4.w;
+  }
+  float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  gemm_col4<EPI>(p, tile_n * BN + 4 * c4, bias, gate);
+  gemm_store4<EPI>(p, row, tile_n * BN + 4 * c4, v, bias, gate);
+}
+
+template <int BM, int BN, int WM, int WN, int NS, int BK, int EPI>
+hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream) {
+  typedef GemmCfg<BM, BN, WM, WN, NS, BK> C;
+  const int tiles = ((a.M + BM - 1) / BM) * (a.N / BN);
+  const int nk = a.K / BK;
+  // Tiles beyond the last full round (one workgroup per CU) are split along
+  // k so that together they fill that round; a reduce kernel adds the splits.
+  const int ncu = device_cu_count();
+  const int tail = tiles % ncu;
+  int nsplit = tail > 0 ? ncu / tail : 1;
+  nsplit = nsplit < nk ? nsplit : nk;
+  const size_t unit_bytes = sizeof(float) * BM * BN;
+  while (nsplit > 1 && static_cast<size_t>(tail) * nsplit * unit_bytes > a.part_bytes) --nsplit;
+  if (a.part == nullptr) nsplit = 1;
+  ::echo::TimedLaunch scope(name, stream);
+  a.tile_base = 0;
+  if (nsplit < 2) {
+    a.nsplit = 1;
+    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI>), dim3(tiles), dim3(C::kThreads), 0, stream, a);
+    return hipGetLastError();
+  }
+  a.kps = (nk + nsplit - 1) / nsplit;  // k-steps per split
+  nsplit = (nk + a.kps - 1) / a.kps;   // every split non-empty
+  const int full = tiles - tail;
+  if (full > 0) {
+    a.nsplit = 1;
+    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI>), dim3(full), dim3(C::kThreads), 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  a.tile_base = full;
+  a.nsplit = nsplit;
+  hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI>), dim3(tail * nsplit), dim3(C::kThreads), 0,
+                     stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t threads = static_cast<int64_t>(tail) * BM * (BN / 4);
+  hipLaunchKernelGGL((gemm_splitk_reduce<BM, BN, EPI>), dim3(static_cast<unsigned>((threads + 255) / 256)),
+                     dim3(256), 0, stream, a, tail);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int WM, int WN, int NS, int BK>
 hipError_t launch_gemm_tile(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream) {
-  typedef GemmCfg<BM, BN, WM, WN, NS, BK> C;
   if (a.N % BN != 0 || (a.n_split < a.N && a.n_split % BN != 0) || a.K % BK != 0)
     return hipErrorInvalidValue;
-  const int tiles = ((a.M + BM - 1) / BM) * (a.N / BN);
-  const dim3 grid(tiles), block(C::kThreads);
   switch (epi) {
-    case EPI_BIAS:
-      return ECHO_LAUNCH(name, (gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI_BIAS>), grid, block, 0, stream, a);
-    case EPI_GELU:
-      return ECHO_LAUNCH(name, (gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI_GELU>), grid, block, 0, stream, a);
-    default:
-      return ECHO_LAUNCH(name, (gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI_GATE_RES>), grid, block, 0, stream, a);
+    case EPI_BIAS: return launch_gemm_epi<BM, BN, WM, WN, NS, BK, EPI_BIAS>(name, a, stream);
+    case EPI_GELU: return launch_gemm_epi<BM, BN, WM, WN, NS, BK, EPI_GELU>(name, a, stream);
+    default: return launch_gemm_epi<BM, BN, WM, WN, NS, BK, EPI_GATE_RES>(name, a, stream);
   }
 }
 

@@ -31,6 +31,11 @@ struct GemmBf16Args {
   int64_t ldr;
   const int32_t* res_rows;  // optional gather of residual rows
   int res_bf16;
+  float* part;              // optional: fp32 partial tiles of the split-K tail
+  size_t part_bytes;
+  // set by the launcher: first tile of a launch, k splits per tile (<= 1: the
+  // whole k range), k-steps per split
+  int tile_base, nsplit, kps;
 };
 
 struct GemmF32Args {
@@ -80,6 +85,11 @@ hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
                             float* part, size_t part_bytes, hipStream_t stream);
 size_t attn_partial_bytes();
+// bytes that hold the partial results of any split tail of the bf16 block
+// (attention key splits, GEMM k splits): 256 units of the larger kind
+size_t block_partial_bytes();
+// compute units of the current device (cached; 256 if the query fails)
+int device_cu_count();
 hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, const float* v, int64_t ldkv,
                            int Mq, int L, int H, int dh, float* out, int64_t ldo, hipStream_t stream);
 
