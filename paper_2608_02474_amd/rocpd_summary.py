@@ -6,8 +6,9 @@ with its default output format).
     python -m paper_2608_02474_amd.rocpd_summary counter RESULTS.db COUNTER
         per (kernel, grid size): dispatches and the average counter value
     python -m paper_2608_02474_amd.rocpd_summary traffic FETCH.db WRITE.db \
-            COPY_FETCH.db COPY_WRITE.db KEY=KERNEL_SUBSTRING@GRID@SOURCE ...
-        HBM bytes per launch of each named (kernel, grid), calibrated with the
+            COPY_FETCH.db COPY_WRITE.db KEY=KERNEL_SUBSTRING@GRID[+KERNEL_SUBSTRING@GRID...]@SOURCE ...
+        HBM bytes per call of each named (kernel, grid) or sum of them (a call
+        made of several launches), calibrated with the
         counters of a copy of known size (the hbm_copy module: 1 GiB read and
         1 GiB written), as JSON records keyed KEY carrying the sha256 of SOURCE
         (the kernel's source file, so that a stale record can be recognised)
@@ -70,13 +71,18 @@ def traffic(fetch_db, write_db, copy_fetch_db, copy_write_db, specs):
     out = {}
     for spec in specs:
         key, rest = spec.split("=", 1)
-        sub, grid, source = rest.split("@")
-        f = counter_of(fetch_db, "FETCH_SIZE", sub, int(grid))
-        w = counter_of(write_db, "WRITE_SIZE", sub, int(grid))
+        parts, source = rest.rsplit("@", 1)
+        f = w = 0.0
+        grids = []
+        for part in parts.split("+"):
+            sub, grid = part.rsplit("@", 1)
+            f += counter_of(fetch_db, "FETCH_SIZE", sub, int(grid))
+            w += counter_of(write_db, "WRITE_SIZE", sub, int(grid))
+            grids.append(int(grid))
         out[key] = {"fetch_kib": round(f, 1), "write_kib": round(w, 1),
                     "fetch_factor": round(ff, 4), "write_factor": round(wf, 4),
                     "bytes_per_launch": int(round((f * ff + w * wf) * 1024)),
-                    "grid_threads": int(grid),
+                    "grid_threads": grids[0] if len(grids) == 1 else grids,
                     "source_sha256": hashlib.sha256(open(source, "rb").read()).hexdigest()}
     return out
 
