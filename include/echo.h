@@ -205,6 +205,60 @@ int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* i
                       const uint8_t* mask, int32_t n_sel, const float* y_sel,
                       void* xref, int8_t* codes, float* scale, void* y, void* stream);
 
+/* ---------------------------------------------- adaptive reference cache */
+/*
+ * The paper's memory-efficient cache (Sec. 3.4, "Memory-efficient Cache
+ * Management") in place of echo_cache_update's one-reference-per-token form:
+ * a fresh output y whose cosine similarity <y, r> / (|y| |r|) with its chain's
+ * current reference r exceeds tau is kept as an int8 residual against r
+ * (res = fp32(y - r), codes and scale as in echo_cache_update); otherwise y
+ * itself is stored in `dtype` and becomes the chain's current reference.  A
+ * chain is chain_len consecutive tokens (one spatial row of the latent grid)
+ * and keeps its current reference across updates; the similarity is taken in
+ * fp64 (0 if a norm is 0) and compared strictly.  Before the write, the old
+ * entries of the rewritten tokens are dropped; a reference that no entry and
+ * no chain holds any more is released to the free slots.
+ *
+ * Fusion: selected row i = idx[j] outputs cast(y_sel[j]) and records
+ * xref_i = x_i (the saliency reference of echo_select); an unselected row
+ * outputs its reference row, or cast(fp32(r + fp32(scale_i * code))) for a
+ * residual entry, or zeros if it never had an entry.
+ *
+ * State: caller-owned device arrays (echo_refcache_state), prepared once by
+ * echo_refcache_init.  capacity >= L + L / chain_len reference slots always
+ * suffice (every live slot is held by an entry or a chain).  The number of
+ * live references is capacity - *free_top.  x, xref, y: [L][D] `dtype`;
+ * idx [n_sel] ascending distinct rows with mask their indicator; y_sel
+ * [n_sel][D] fp32.  Requires L % chain_len == 0, D % 8 == 0, D <= 16384, tau
+ * finite.  Slot numbers depend on the order of atomic operations; stored
+ * values, decisions and outputs do not.
+ */
+typedef struct {
+  int32_t L;
+  int32_t D;
+  int32_t dtype;
+  int32_t chain_len;
+  int32_t capacity;
+  float tau;
+} echo_refcache_cfg;
+
+typedef struct {
+  void* pool;          /* [capacity][D] `dtype`: reference rows */
+  int32_t* refcount;   /* [capacity] holders of each slot */
+  int32_t* free_list;  /* [capacity] stack of free slots */
+  int32_t* free_top;   /* [1] number of free slots */
+  int32_t* chain_ref;  /* [L / chain_len] current reference slot, -1 = none */
+  int32_t* ent_slot;   /* [L] slot of the token's entry, -1 = none */
+  uint8_t* ent_kind;   /* [L] 0 none, 1 reference, 2 residual */
+  int8_t* codes;       /* [L][D] residual codes */
+  float* scale;        /* [L] residual scales */
+} echo_refcache_state;
+
+int echo_refcache_init(const echo_refcache_cfg* cfg, const echo_refcache_state* st, void* stream);
+int echo_refcache_update(const echo_refcache_cfg* cfg, const echo_refcache_state* st, const void* x,
+                         const int32_t* idx, const uint8_t* mask, int32_t n_sel,
+                         const float* y_sel, void* xref, void* y, void* stream);
+
 /* ------------------------------------------------------------ kernel timing */
 /*
  * Optional per-kernel timing with HIP events, for the calling thread.

@@ -59,7 +59,9 @@ class RefCache:
 
     def __init__(self, L: int, D: int, chain_len: int, tau: float, dtype: str):
         assert L % chain_len == 0
-        self.L, self.D, self.chain_len, self.tau, self.dtype = L, D, chain_len, float(tau), dtype
+        # the threshold is an fp32 value (the boundary passes it as a float)
+        self.L, self.D, self.chain_len, self.dtype = L, D, chain_len, dtype
+        self.tau = float(np.float32(tau))
         self.refs: dict[int, np.ndarray] = {}   # reference id -> stored row (fp32 values)
         self.holds: dict[int, int] = {}         # reference id -> number of holders
         self.kind = np.zeros(L, np.int8)

@@ -46,6 +46,16 @@ class CacheCfg(ctypes.Structure):
     _fields_ = [("L", c_int32), ("D", c_int32), ("dtype", c_int32)]
 
 
+class RefCacheCfg(ctypes.Structure):
+    _fields_ = [("L", c_int32), ("D", c_int32), ("dtype", c_int32), ("chain_len", c_int32),
+                ("capacity", c_int32), ("tau", c_float)]
+
+
+class RefCacheState(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("pool", "refcount", "free_list", "free_top", "chain_ref",
+                                        "ent_slot", "ent_kind", "codes", "scale")]
+
+
 class KernelTime(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char_p), ("launches", c_int64), ("total_ms", c_double)]
 
@@ -68,6 +78,10 @@ _SIGNATURES = {
     "echo_cache_update": (ctypes.c_int, [_P(CacheCfg), c_void_p, c_void_p, c_void_p, c_int32,
                                          c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                          c_void_p]),
+    "echo_refcache_init": (ctypes.c_int, [_P(RefCacheCfg), _P(RefCacheState), c_void_p]),
+    "echo_refcache_update": (ctypes.c_int, [_P(RefCacheCfg), _P(RefCacheState), c_void_p,
+                                            c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
+                                            c_void_p, c_void_p]),
     "echo_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "echo_profile_read": (ctypes.c_int, [_P(KernelTime), c_int32]),
 }

@@ -20,7 +20,8 @@ import math
 import torch
 
 from . import _lib
-from ._lib import (BlockCfg, BlockWeights, CacheCfg, EnergyCfg, KernelTime, SelectCfg,
+from ._lib import (BlockCfg, BlockWeights, CacheCfg, EnergyCfg, KernelTime, RefCacheCfg,
+                   RefCacheState, SelectCfg,
                    ECHO_BF16, ECHO_F32, check)
 
 _DTYPES = {torch.float32: ECHO_F32, torch.bfloat16: ECHO_BF16}
@@ -227,6 +228,65 @@ def cache_update(x: torch.Tensor, idx: torch.Tensor, mask: torch.Tensor, n_sel: 
                                 _ptr(mask), n_sel, _ptr(y_sel) if n_sel else None, _ptr(xref),
                                 _ptr(codes), _ptr(scale), _ptr(y), _stream()))
     return y
+
+
+# ---------------------------------------------------- adaptive reference cache
+
+class RefCache:
+    """Device state of the adaptive reference cache (Sec. 3.4): reference pool
+    with hold counts and free slots, per-token entries (kind, slot, int8
+    residual codes, scale) and each chain's current reference."""
+
+    def __init__(self, L: int, D: int, chain_len: int, tau: float, dtype, device,
+                 capacity: int | None = None):
+        if L % chain_len:
+            raise ValueError("L must be a multiple of chain_len")
+        self.L, self.D, self.chain_len, self.tau, self.dtype = L, D, chain_len, float(tau), dtype
+        self.n_chains = L // chain_len
+        self.capacity = capacity if capacity is not None else L + self.n_chains
+        kw = dict(device=device)
+        self.pool = torch.empty((self.capacity, D), dtype=dtype, **kw)
+        self.refcount = torch.empty(self.capacity, dtype=torch.int32, **kw)
+        self.free_list = torch.empty(self.capacity, dtype=torch.int32, **kw)
+        self.free_top = torch.empty(4, dtype=torch.int32, **kw)  # [0] used; 16-byte alignment
+        self.chain_ref = torch.empty(self.n_chains, dtype=torch.int32, **kw)
+        self.ent_slot = torch.empty(L, dtype=torch.int32, **kw)
+        self.ent_kind = torch.empty(L, dtype=torch.uint8, **kw)
+        self.codes = torch.empty((L, D), dtype=torch.int8, **kw)
+        self.scale = torch.empty(L, dtype=torch.float32, **kw)
+        self.cfg = RefCacheCfg(L, D, _echo_dtype(self.pool), chain_len, self.capacity, self.tau)
+        self.state = RefCacheState(*[_ptr(t) for t in (self.pool, self.refcount, self.free_list,
+                                                        self.free_top, self.chain_ref, self.ent_slot,
+                                                        self.ent_kind, self.codes, self.scale)])
+        check("echo_refcache_init",
+              _lib_handle().echo_refcache_init(ctypes.byref(self.cfg), ctypes.byref(self.state),
+                                               _stream()))
+
+    def update(self, x: torch.Tensor, idx: torch.Tensor, mask: torch.Tensor, n_sel: int,
+               y_sel: torch.Tensor, xref: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+        """Writes the fresh rows, records their inputs in xref; returns the fused y."""
+        _dev(x, "x", self.dtype)
+        _dev(mask, "mask", torch.uint8)
+        _dev(xref, "xref", self.dtype)
+        if n_sel > 0:
+            _dev(idx, "idx", torch.int32)
+            _dev(y_sel, "y_sel", torch.float32)
+        if y is None:
+            y = torch.empty_like(x)
+        check("echo_refcache_update",
+              _lib_handle().echo_refcache_update(
+                  ctypes.byref(self.cfg), ctypes.byref(self.state), _ptr(x),
+                  _ptr(idx) if n_sel else None, _ptr(mask), n_sel,
+                  _ptr(y_sel) if n_sel else None, _ptr(xref), _ptr(y), _stream()))
+        return y
+
+    def live_refs(self) -> int:
+        """References currently held (synchronizes with the device)."""
+        return self.capacity - int(self.free_top[0].item())
+
+    def live_bytes(self) -> int:
+        """Bytes of live cache state: held reference rows plus codes and scales."""
+        return self.live_refs() * self.D * self.pool.element_size() + self.codes.numel() + 4 * self.L
 
 
 # ------------------------------------------------------------- kernel timing

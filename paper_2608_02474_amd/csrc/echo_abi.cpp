@@ -5,6 +5,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <cmath>
 #include <vector>
 
 #include "../../include/echo.h"
@@ -349,6 +350,39 @@ int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* i
   return device_status(launch_cache_update(cfg->dtype == ECHO_BF16, x, idx, mask, n_sel, cfg->L, cfg->D,
                                            y_sel, xref, codes, scale, y,
                                            static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+bool refcache_cfg_ok(const echo_refcache_cfg* c) {
+  return c != nullptr && c->L >= 1 && c->D >= 8 && (c->D % 8) == 0 && c->D <= 16384 && ok_dtype(c->dtype) &&
+         c->chain_len >= 1 && (c->L % c->chain_len) == 0 && std::isfinite(c->tau) &&
+         static_cast<int64_t>(c->capacity) >= static_cast<int64_t>(c->L) + c->L / c->chain_len;
+}
+bool refcache_state_ok(const echo_refcache_state* s) {
+  return s != nullptr && ok_ptr(s->pool) && ok_ptr(s->refcount) && ok_ptr(s->free_list) && ok_ptr(s->free_top) &&
+         ok_ptr(s->chain_ref) && ok_ptr(s->ent_slot) && ok_ptr(s->ent_kind) && ok_ptr(s->codes) &&
+         ok_ptr(s->scale);
+}
+}  // namespace
+
+int echo_refcache_init(const echo_refcache_cfg* cfg, const echo_refcache_state* st, void* stream) {
+  if (!refcache_cfg_ok(cfg) || !refcache_state_ok(st)) return ECHO_EINVAL;
+  return device_status(launch_refcache_init(cfg->L, cfg->L / cfg->chain_len, cfg->capacity, st->refcount,
+                                            st->free_list, st->free_top, st->chain_ref, st->ent_slot,
+                                            st->ent_kind, st->scale, static_cast<hipStream_t>(stream)));
+}
+
+int echo_refcache_update(const echo_refcache_cfg* cfg, const echo_refcache_state* st, const void* x,
+                         const int32_t* idx, const uint8_t* mask, int32_t n_sel, const float* y_sel,
+                         void* xref, void* y, void* stream) {
+  if (!refcache_cfg_ok(cfg) || !refcache_state_ok(st)) return ECHO_EINVAL;
+  if (n_sel < 0 || n_sel > cfg->L) return ECHO_EINVAL;
+  if (!ok_ptr(x) || !ok_ptr(mask) || !ok_ptr(xref) || !ok_ptr(y)) return ECHO_EINVAL;
+  if (n_sel > 0 && (!ok_ptr(idx) || !ok_ptr(y_sel))) return ECHO_EINVAL;
+  return device_status(launch_refcache_update(
+      cfg->dtype == ECHO_BF16, x, idx, mask, n_sel, cfg->L, cfg->D, cfg->chain_len, cfg->tau, y_sel, st->pool,
+      st->refcount, st->free_list, st->free_top, st->chain_ref, st->ent_slot, st->ent_kind, st->codes,
+      st->scale, xref, y, static_cast<hipStream_t>(stream)));
 }
 
 int echo_profile_enable(int on) {

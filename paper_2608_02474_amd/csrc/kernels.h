@@ -71,6 +71,15 @@ hipError_t launch_cache_update(int dtype_bf16, const void* x, const int32_t* idx
                                int n_sel, int L, int D, const float* y_sel, void* xref, int8_t* codes,
                                float* scale, void* y, hipStream_t stream);
 
+hipError_t launch_refcache_init(int L, int n_chains, int capacity, int32_t* refcount, int32_t* free_list,
+                                int32_t* free_top, int32_t* chain_ref, int32_t* ent_slot, uint8_t* ent_kind,
+                                float* scale, hipStream_t stream);
+hipError_t launch_refcache_update(int dtype_bf16, const void* x, const int32_t* idx, const uint8_t* mask,
+                                  int n_sel, int L, int D, int chain_len, float tau, const float* y_sel,
+                                  void* pool, int32_t* refcount, int32_t* free_list, int32_t* free_top,
+                                  int32_t* chain_ref, int32_t* ent_slot, uint8_t* ent_kind, int8_t* codes,
+                                  float* scale, void* xref, void* y, hipStream_t stream);
+
 hipError_t launch_modln_input(int dtype_bf16, const void* x, int M, int D, const float* shift,
                               const float* scale, float eps, void* out, hipStream_t stream);
 hipError_t launch_modln_x1(int dtype_bf16, const float* x1, int M, int D, const float* shift,

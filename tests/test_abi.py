@@ -88,8 +88,8 @@ def test_block_rejects_before_launch(lib):
     assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6), wsb=64) == _lib.ECHO_EWORKSPACE
     bad = _lib.BlockWeights(*([0x20000] * 12 + [0x20008]))                            # misaligned mod
     assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6), weights=bad) == _lib.ECHO_EINVAL
-    # n_sel == 0 is a successful no-op that launches nothing
     assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6, 2)) == _lib.ECHO_EINVAL      # unknown flag
+    # n_sel == 0 is a successful no-op that launches nothing
     assert run(_lib.BlockCfg(32, 256, 2, 512, bf, 1e-6), n=0) == _lib.ECHO_OK
 
 
@@ -107,3 +107,22 @@ def test_profile_read_empty(lib):
     arr = (_lib.KernelTime * 4)()
     assert lib.echo_profile_read(arr, 4) == 0
     assert lib.echo_profile_read(None, -1) == -_lib.ECHO_EINVAL
+
+
+def test_refcache_rejects_before_launch(lib):
+    st = _lib.RefCacheState(*([0x20000] * 9))
+    def run(cfg, n=4, state=st, x=FAKE):
+        return lib.echo_refcache_update(ctypes.byref(cfg), ctypes.byref(state), x, FAKE, FAKE, n,
+                                        FAKE, FAKE, FAKE, None)
+    ok = _lib.RefCacheCfg(40, 64, 0, 8, 45, 0.5)
+    assert run(_lib.RefCacheCfg(40, 64, 0, 7, 46, 0.5)) == _lib.ECHO_EINVAL            # L % chain_len
+    assert run(_lib.RefCacheCfg(40, 64, 0, 8, 44, 0.5)) == _lib.ECHO_EINVAL            # capacity < L + chains
+    assert run(_lib.RefCacheCfg(40, 60, 0, 8, 45, 0.5)) == _lib.ECHO_EINVAL            # D % 8
+    assert run(_lib.RefCacheCfg(40, 64, 0, 8, 45, float("nan"))) == _lib.ECHO_EINVAL   # tau
+    assert run(_lib.RefCacheCfg(40, 64, 5, 8, 45, 0.5)) == _lib.ECHO_EINVAL            # dtype
+    assert run(ok, n=41) == _lib.ECHO_EINVAL
+    assert run(ok, x=MISALIGNED) == _lib.ECHO_EINVAL
+    bad = _lib.RefCacheState(*([0x20000] * 8 + [0]))                                   # null scale
+    assert run(ok, state=bad) == _lib.ECHO_EINVAL
+    assert lib.echo_refcache_init(ctypes.byref(_lib.RefCacheCfg(40, 64, 0, 8, 44, 0.5)),
+                                  ctypes.byref(st), None) == _lib.ECHO_EINVAL

@@ -143,14 +143,21 @@ def test_step_update_fuses_fresh_and_cached():
 
 
 def test_threshold_is_strict():
-    # cos((3, 4), (4, 3)) = 24 / 25: equal to tau -> a new reference; just above -> residual
-    y = np.array([[3, 4], [4, 3]], np.float32)
-    c = RefCache(2, 2, 2, tau=0.96, dtype="f32")
+    # cos(e1, (1, 1, 1, 1)) = 1 / 2 exactly (norms 1 and 2): equal to tau -> a new
+    # reference; a threshold just below -> residual
+    y = np.array([[1, 0, 0, 0], [1, 1, 1, 1]], np.float32)
+    c = RefCache(2, 4, 2, tau=0.5, dtype="f32")
     c.write([0, 1], y)
+    assert c.sims[1] == 0.5
     assert list(c.kind) == [REFERENCE, REFERENCE]
-    c = RefCache(2, 2, 2, tau=0.9599, dtype="f32")
+    c = RefCache(2, 4, 2, tau=0.4999, dtype="f32")
     c.write([0, 1], y)
     assert list(c.kind) == [REFERENCE, RESIDUAL]
+
+
+def test_threshold_is_the_fp32_value():
+    # the boundary takes tau as an fp32: 0.3 means 0.30000001192...
+    assert RefCache(2, 4, 2, tau=0.3, dtype="f32").tau == float(np.float32(0.3))
 
 
 def test_current_reference_persists_across_writes():
