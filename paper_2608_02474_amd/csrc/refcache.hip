@@ -17,7 +17,7 @@
 //                     the chain still held is reused in place);
 //   refcache_fuse     one wave per row: fresh rows output cast(y_sel) and
 //                     record their input as the saliency reference; the
-//                     others are rebuilt from their entry.
+//                     others are rebuilt from their entry (16-byte accesses).
 // Every live slot is held by a token entry or a chain, so capacity >= L +
 // number of chains never runs out.  Slot numbers depend on the order of the
 // atomic pops; stored values and decisions do not.
@@ -146,21 +146,21 @@ refcache_write(const int32_t* __restrict__ idx, int n_sel, const float* __restri
   }
 
   float y[U][4];
-  auto load_y = [&](int j) __attribute__((always_inline)) {
+  float4 ynext[U];  // the next token's row, loaded while this one is processed
+  auto fetch = [&](int j) __attribute__((always_inline)) {
     const float* yp = y_sel + static_cast<int64_t>(j) * D;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (col(u) < D) {
-        const float4 v = *reinterpret_cast<const float4*>(yp + col(u));
-        y[u][0] = v.x; y[u][1] = v.y; y[u][2] = v.z; y[u][3] = v.w;
-      } else {
-        y[u][0] = y[u][1] = y[u][2] = y[u][3] = 0.0f;
-      }
-    }
+    for (int u = 0; u < U; ++u)
+      ynext[u] = col(u) < D ? *reinterpret_cast<const float4*>(yp + col(u)) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
   };
-  load_y(j0);
+  fetch(j0);
   for (int j = j0; j < j1; ++j) {
     const int l = idx[j];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      y[u][0] = ynext[u].x; y[u][1] = ynext[u].y; y[u][2] = ynext[u].z; y[u][3] = ynext[u].w;
+    }
+    if (j + 1 < j1) fetch(j + 1);
     bool residual = false;
     if (cr >= 0) {
       double dot = 0.0, yy = 0.0;
@@ -237,10 +237,7 @@ refcache_write(const int32_t* __restrict__ idx, int n_sel, const float* __restri
         sh_slot = s;
       }
       __syncthreads();
-      if (sh_slot < 0) {
-        if (j + 1 < j1) load_y(j + 1);
-        continue;
-      }
+      if (sh_slot < 0) continue;
       cr = sh_slot;
       T* rp = pool + static_cast<int64_t>(cr) * D;
       double s = 0.0;
@@ -255,12 +252,12 @@ refcache_write(const int32_t* __restrict__ idx, int n_sel, const float* __restri
       }
       rr = block_sum(s, red_d[0]);
     }
-    if (j + 1 < j1) load_y(j + 1);
   }
 }
 
 // waves [0, n_sel): fresh row idx[j]; waves [n_sel, n_sel + L): row i reads
-// its entry if mask[i] == 0
+// its entry if mask[i] == 0.  8-element chunks with 16-byte accesses, four
+// chunks' loads issued before any is used.
 template <typename T>
 __global__ void __launch_bounds__(kRcThreads)
 refcache_fuse(const T* __restrict__ x, const int32_t* __restrict__ idx, const uint8_t* __restrict__ mask,
@@ -268,18 +265,35 @@ refcache_fuse(const T* __restrict__ x, const int32_t* __restrict__ idx, const ui
               const int32_t* __restrict__ ent_slot, const uint8_t* __restrict__ ent_kind,
               const int8_t* __restrict__ codes, const float* __restrict__ scale, T* __restrict__ xref,
               T* __restrict__ y) {
+  constexpr int B = 4;  // chunks in flight per lane
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t g = static_cast<int64_t>(blockIdx.x) * kRcWaves + wave;
+  const int nch = D / 8;
   if (g < n_sel) {
     const int64_t i = idx[g];
-    for (int c = lane * 4; c < D; c += kWave * 4) {
-      const float4 v = *reinterpret_cast<const float4*>(y_sel + g * D + c);
-      Elem<T>::store(y, i * D + c, v.x);
-      Elem<T>::store(y, i * D + c + 1, v.y);
-      Elem<T>::store(y, i * D + c + 2, v.z);
-      Elem<T>::store(y, i * D + c + 3, v.w);
+    const float* ys = y_sel + g * D;
+    for (int c0 = lane; c0 < nch; c0 += B * kWave) {
+      Raw8<float> yr[B];
+      Raw8<T> xr[B];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) xref[i * D + c + e] = x[i * D + c + e];
+      for (int u = 0; u < B; ++u) {
+        const int c = c0 + u * kWave;
+        if (c < nch) {
+          yr[u].load(ys + c * 8);
+          xr[u].load(x + i * D + c * 8);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int c = c0 + u * kWave;
+        if (c < nch) {
+          float v[8];
+          yr[u].unpack(v);
+          stg16(y + i * D + c * 8, pack16(v, static_cast<const T*>(nullptr)));
+          if (sizeof(T) == 4) stg16(y + i * D + c * 8 + 4, pack16(v + 4, static_cast<const T*>(nullptr)));
+          xr[u].store(xref + i * D + c * 8);
+        }
+      }
     }
     return;
   }
@@ -288,16 +302,33 @@ refcache_fuse(const T* __restrict__ x, const int32_t* __restrict__ idx, const ui
   const int kind = ent_kind[i];
   const T* rp = pool + static_cast<int64_t>(ent_slot[i] < 0 ? 0 : ent_slot[i]) * D;
   const float sc = scale[i];
-  for (int c = lane * 4; c < D; c += kWave * 4) {
+  for (int c0 = lane; c0 < nch; c0 += B * kWave) {
+    Raw8<T> rr[B];
+    uint2 cw[B];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      float v = 0.0f;
-      if (kind == 1) {
-        v = Elem<T>::load(rp, c + e);
-      } else if (kind == 2) {
-        v = mul_add_rn(sc, static_cast<float>(codes[i * D + c + e]), Elem<T>::load(rp, c + e));
+    for (int u = 0; u < B; ++u) {
+      const int c = c0 + u * kWave;
+      if (c < nch && kind != 0) {
+        rr[u].load(rp + c * 8);
+        cw[u] = *reinterpret_cast<const uint2*>(codes + i * D + c * 8);
       }
-      Elem<T>::store(y, i * D + c + e, v);
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int c = c0 + u * kWave;
+      if (c >= nch) continue;
+      float v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+      if (kind != 0) rr[u].unpack(v);
+      if (kind == 2) {
+        const uint32_t w[2] = {cw[u].x, cw[u].y};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int8_t q = static_cast<int8_t>((w[e / 4] >> (8 * (e % 4))) & 0xffu);
+          v[e] = mul_add_rn(sc, static_cast<float>(q), v[e]);
+        }
+      }
+      stg16(y + i * D + c * 8, pack16(v, static_cast<const T*>(nullptr)));
+      if (sizeof(T) == 4) stg16(y + i * D + c * 8 + 4, pack16(v + 4, static_cast<const T*>(nullptr)));
     }
   }
 }
