@@ -189,12 +189,68 @@ def refcache_leg(w, dev, dt, steps: int = 5, tau: float = 0.9, corr: float = 0.9
                     "latent-grid row"}
 
 
+def stack_leg(w, dev, dt, fw, n_blocks: int, steps: int, n_full: int = 2, r_min: float = 0.2,
+              r_max: float = 0.6, alpha: float = 0.4):
+    """A stack of n_blocks blocks of the workload's shape over a synthetic
+    denoising trajectory of first-block inputs x_{t+1} = x_t + (0.3 / (t + 1)) N(0, 1):
+    one Eq. 1 value and one selection per step on the first block's input, K from
+    the step schedule, then every block on the shared selection.  Random-init
+    weights (generated on the device, same distributions as the main step)."""
+    import torch
+
+    from paper_2608_02474_amd import api
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(2000 + w.seed)
+    D, F = w.D, w.F
+
+    def rnd(*shape, std=0.02, mean=0.0, dtype=dt):
+        return (torch.randn(shape, device=dev, generator=g) * std + mean).to(dtype)
+
+    blocks = []
+    for _ in range(n_blocks):
+        mod = torch.cat([rnd(2, D, std=0.1, dtype=torch.float32), rnd(1, D, std=0.05, mean=0.25, dtype=torch.float32),
+                         rnd(2, D, std=0.1, dtype=torch.float32), rnd(1, D, std=0.05, mean=0.25, dtype=torch.float32)])
+        blocks.append({"wq": rnd(D, D), "wk": rnd(D, D), "wv": rnd(D, D), "wo": rnd(D, D),
+                       "w1": rnd(F, D), "w2": rnd(D, F), "bq": rnd(D), "bk": rnd(D), "bv": rnd(D),
+                       "bo": rnd(D), "b1": rnd(F), "b2": rnd(D), "mod": mod.contiguous()})
+    stack = api.BlockStack(blocks, w.H, w.L, D, dev, dt, api.Scheduler(n_full, r_min, r_max, alpha))
+    x = torch.randn((w.L, D), device=dev, generator=g)
+    times = []
+    for t in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        stack.step(x.to(dt), fw, w.N)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+        x = x + torch.randn((w.L, D), device=dev, generator=g) * (0.3 / (t + 1))
+    ks = [k for k, _, _ in stack.history]
+    full = [f for _, f, _ in stack.history]
+    full_ms = [tm for tm, f in zip(times, full) if f]
+    cached_ms = [tm for tm, f in zip(times, full) if not f]
+    ref = sum(full_ms) / len(full_ms)
+    return {"blocks": n_blocks, "steps": steps,
+            "schedule": {"n_full": n_full, "r_min": r_min, "r_max": r_max, "alpha": alpha},
+            "k_per_step": ks, "full_step": full,
+            "delta_per_step": [None if f else round(d, 6) for _, f, d in stack.history],
+            "ms_per_step": [round(tm, 2) for tm in times],
+            "full_step_ms": round(ref, 2),
+            "cached_step_ms_mean": round(sum(cached_ms) / max(len(cached_ms), 1), 2),
+            "trajectory_ms": round(sum(times), 1),
+            "speedup_vs_all_full": round(ref * steps / sum(times), 3),
+            "data": "synthetic trajectory and random-init weights (device-generated)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="wan14b_480p_32760tok")
+    ap.add_argument("--stack-blocks", type=int, default=40,
+                    help="blocks of the stack leg (the scheduled multi-block trajectory); 0: skip")
+    ap.add_argument("--stack-steps", type=int, default=10)
     ap.add_argument("--skip-cpu-baseline", action="store_true",
                     help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
                          "unchanged")
@@ -310,6 +366,12 @@ def main() -> int:
 
     log("adaptive reference cache leg")
     out["refcache"] = refcache_leg(w, dev, dt)
+    if args.stack_blocks > 0:
+        log(f"stack leg: {args.stack_blocks} blocks, {args.stack_steps} steps")
+        blk = None                             # free the main step's block and workspace
+        torch.cuda.empty_cache()
+        _, _, fw_stack = api.energy(A, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
+        out["stack"] = stack_leg(w, dev, dt, fw_stack, args.stack_blocks, args.stack_steps)
 
     if args.skip_cpu_baseline:
         out["cpu_baseline"] = None

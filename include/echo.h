@@ -126,6 +126,54 @@ int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref,
                 float* saliency, double* step_delta,
                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * The two halves of echo_select, for callers that choose k from the step's
+ * Eq. 1 value (the step schedule below): echo_saliency computes the saliency
+ * (and, if step_delta is not NULL, the Eq. 1 value); echo_topk selects from a
+ * given saliency with cfg->k / cfg->threshold as echo_select does.  Running
+ * both gives exactly echo_select's results.  echo_saliency's workspace is
+ * echo_saliency_workspace(cfg) bytes; echo_topk needs none.
+ */
+size_t echo_saliency_workspace(const echo_select_cfg* cfg);
+int echo_saliency(const echo_select_cfg* cfg, const void* x, const void* xref,
+                  const float* frame_weight, float* saliency, double* step_delta,
+                  void* workspace, size_t workspace_bytes, void* stream);
+int echo_topk(const echo_select_cfg* cfg, const float* saliency, int32_t* idx, uint8_t* mask,
+              int32_t* n_sel, void* stream);
+
+/* ---------------------------------------------------------- step schedule */
+/*
+ * Step-level cache schedule (Sec. 3.3, "Energy-Guided Step-Latent Cache
+ * Scheduling"; Sec. 3.1 Eq. 2).  Host function: no device work.  Decides step
+ * st->step and advances the state:
+ *   step < n_full                     -> full step (k = L);
+ *   otherwise acc += delta_t; if refresh_delta > 0 and acc > refresh_delta
+ *                                     -> full step, acc = 0 (Eq. 2 refresh);
+ *   otherwise dmax = max(dmax, delta_t); dhat = delta_t / dmax (0 if dmax == 0);
+ *             r = clip(r_min + alpha * dhat, r_min, r_max);
+ *             k = ceil(r * L - 1e-9), clamped to [0, L].
+ * delta_t is the step's Eq. 1 value (echo_saliency's step_delta); it is not
+ * used on the leading full steps.  Returns k, or -ECHO_EINVAL for a bad
+ * argument (L < 1, r_min > r_max, a rate outside [0, 1], NULL pointers).
+ * *full is set to 1 for a full step, else 0.
+ */
+typedef struct {
+  int32_t n_full;        /* leading full steps */
+  double r_min;          /* minimum and maximum update ratio */
+  double r_max;
+  double alpha;          /* adjustment coefficient */
+  double refresh_delta;  /* Eq. 2 threshold; <= 0: no refresh */
+} echo_schedule_cfg;
+
+typedef struct {
+  int32_t step;          /* steps decided so far (start at 0) */
+  double delta_max;      /* largest delta_t of the cached steps */
+  double delta_acc;      /* delta_t accumulated since the last full step */
+} echo_schedule_state;
+
+int32_t echo_schedule_next(const echo_schedule_cfg* cfg, echo_schedule_state* st, double delta_t,
+                           int32_t L, int32_t* full);
+
 /* ------------------------------------------------------------ block partial */
 /*
  * One adaLN DiT block on the selected tokens only (Sec. 3.3, "Fine-grained

@@ -56,6 +56,15 @@ class RefCacheState(ctypes.Structure):
                                         "ent_slot", "ent_kind", "codes", "scale")]
 
 
+class ScheduleCfg(ctypes.Structure):
+    _fields_ = [("n_full", c_int32), ("r_min", c_double), ("r_max", c_double), ("alpha", c_double),
+                ("refresh_delta", c_double)]
+
+
+class ScheduleState(ctypes.Structure):
+    _fields_ = [("step", c_int32), ("delta_max", c_double), ("delta_acc", c_double)]
+
+
 class KernelTime(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char_p), ("launches", c_int64), ("total_ms", c_double)]
 
@@ -72,6 +81,12 @@ _SIGNATURES = {
     "echo_select": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                    c_void_p]),
+    "echo_saliency_workspace": (c_size_t, [_P(SelectCfg)]),
+    "echo_saliency": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_void_p, c_size_t, c_void_p]),
+    "echo_topk": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+    "echo_schedule_next": (c_int32, [_P(ScheduleCfg), _P(ScheduleState), c_double, c_int32,
+                                     _P(c_int32)]),
     "echo_block_workspace": (c_size_t, [_P(BlockCfg), c_int32]),
     "echo_block_partial": (ctypes.c_int, [_P(BlockCfg), _P(BlockWeights), c_void_p, c_void_p,
                                           c_int32, c_void_p, c_void_p, c_size_t, c_void_p]),

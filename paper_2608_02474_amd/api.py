@@ -21,7 +21,7 @@ import torch
 
 from . import _lib
 from ._lib import (BlockCfg, BlockWeights, CacheCfg, EnergyCfg, KernelTime, RefCacheCfg,
-                   RefCacheState, SelectCfg,
+                   RefCacheState, ScheduleCfg, ScheduleState, SelectCfg,
                    ECHO_BF16, ECHO_F32, check)
 
 _DTYPES = {torch.float32: ECHO_F32, torch.bfloat16: ECHO_BF16}
@@ -153,6 +153,116 @@ def select(x: torch.Tensor, xref: torch.Tensor, frame_weight: torch.Tensor, N: i
                                          _ptr(out.saliency), _ptr(out.step_delta), _ptr(ws),
                                          ws.numel(), _stream()))
     return out
+
+
+def saliency(x: torch.Tensor, xref: torch.Tensor, frame_weight: torch.Tensor, N: int,
+             xi: float = 1e-6, out: Selection | None = None,
+             workspace: Workspace | None = None) -> Selection:
+    """First half of select: saliency and the step's Eq. 1 value (out.saliency,
+    out.step_delta); idx/mask are left for topk."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    _dev(xref, "xref", x.dtype)
+    _dev(frame_weight, "frame_weight", torch.float32)
+    L, D = x.shape
+    if L % N:
+        raise ValueError("L must be a multiple of N")
+    cfg = SelectCfg(L // N, N, D, _echo_dtype(x), 0, 0.0, float(xi))
+    dev = x.device
+    if out is None:
+        out = Selection(idx=torch.empty(L, dtype=torch.int32, device=dev),
+                        mask=torch.empty(L, dtype=torch.uint8, device=dev),
+                        n_sel_dev=torch.empty(1, dtype=torch.int32, device=dev), n_sel=None,
+                        saliency=torch.empty(L, dtype=torch.float32, device=dev),
+                        step_delta=torch.empty(1, dtype=torch.float64, device=dev))
+    need = lib.echo_saliency_workspace(ctypes.byref(cfg))
+    if need == 0:
+        check("echo_saliency", _lib.ECHO_EINVAL)
+    ws = (workspace or _WS["select"]).get(need, dev)
+    check("echo_saliency", lib.echo_saliency(ctypes.byref(cfg), _ptr(x), _ptr(xref), _ptr(frame_weight),
+                                             _ptr(out.saliency), _ptr(out.step_delta), _ptr(ws),
+                                             ws.numel(), _stream()))
+    return out
+
+
+def topk(sel: Selection, N: int, D: int, dtype, k: int | None = None,
+         threshold: float | None = None) -> Selection:
+    """Second half of select: top-k (or threshold) selection from sel.saliency
+    into sel.idx / sel.mask / sel.n_sel_dev."""
+    lib = _lib_handle()
+    L = sel.saliency.numel()
+    if (k is None) == (threshold is None):
+        raise ValueError("pass exactly one of k and threshold")
+    if dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {dtype}")
+    cfg = SelectCfg(L // N, N, D, _DTYPES[dtype], -1 if k is None else int(k),
+                    0.0 if threshold is None else float(threshold), 1e-6)
+    check("echo_topk", lib.echo_topk(ctypes.byref(cfg), _ptr(sel.saliency), _ptr(sel.idx),
+                                     _ptr(sel.mask), _ptr(sel.n_sel_dev), _stream()))
+    sel.n_sel = None if k is None else int(k)
+    return sel
+
+
+class Scheduler:
+    """Step-level cache schedule (echo_schedule_next, a host function)."""
+
+    def __init__(self, n_full: int, r_min: float, r_max: float, alpha: float,
+                 refresh_delta: float = 0.0):
+        self.cfg = ScheduleCfg(int(n_full), float(r_min), float(r_max), float(alpha),
+                               float(refresh_delta))
+        self.state = ScheduleState(0, 0.0, 0.0)
+
+    def next(self, delta_t: float, L: int):
+        """(k, full) for the current step."""
+        full = ctypes.c_int32(0)
+        k = _lib_handle().echo_schedule_next(ctypes.byref(self.cfg), ctypes.byref(self.state),
+                                             float(delta_t), int(L), ctypes.byref(full))
+        if k < 0:
+            check("echo_schedule_next", -k)
+        return int(k), bool(full.value)
+
+
+class BlockStack:
+    """A stack of cached blocks over a denoising trajectory: per step one Eq. 1
+    value and one selection on the first block's input (shared by all blocks),
+    the scheduled K, then block_partial + cache_update block after block."""
+
+    def __init__(self, params: list, H: int, L: int, D: int, device, dtype, scheduler: Scheduler,
+                 xi: float = 1e-6, ln_eps: float = 1e-6):
+        if scheduler.cfg.n_full < 1:
+            raise ValueError("the first step must be a full step (n_full >= 1)")
+        self.params, self.H, self.L, self.D = params, H, L, D
+        self.sched, self.xi, self.ln_eps = scheduler, xi, ln_eps
+        kw = dict(device=device)
+        self.xref = [torch.zeros((L, D), dtype=dtype, **kw) for _ in params]
+        self.codes = [torch.zeros((L, D), dtype=torch.int8, **kw) for _ in params]
+        self.scale = [torch.zeros(L, dtype=torch.float32, **kw) for _ in params]
+        self.y = [torch.empty((L, D), dtype=dtype, **kw) for _ in params]
+        self.y_sel = torch.empty((L, D), dtype=torch.float32, **kw)
+        self.all_idx = torch.arange(L, dtype=torch.int32, **kw)
+        self.all_mask = torch.ones(L, dtype=torch.uint8, **kw)
+        self._w = [block_weights(p) for p in params]
+        self.ws, self.sel_ws, self.sel = Workspace(), Workspace(), None
+        self.history = []   # (k, full, delta_t) per step
+
+    def step(self, x0: torch.Tensor, frame_weight: torch.Tensor, N: int) -> torch.Tensor:
+        self.sel = saliency(x0, self.xref[0], frame_weight, N, self.xi, out=self.sel,
+                            workspace=self.sel_ws)
+        delta_t = float(self.sel.step_delta[0].item())      # host needs it to choose K
+        k, full = self.sched.next(delta_t, self.L)
+        if full:
+            idx, mask, k = self.all_idx, self.all_mask, self.L
+        else:
+            topk(self.sel, N, self.D, x0.dtype, k=k)
+            idx, mask = self.sel.idx, self.sel.mask
+        x = x0
+        for b, p in enumerate(self.params):
+            ys = block_partial(p, x, idx, k, self.H, self.ln_eps, y_sel=self.y_sel,
+                               workspace=self.ws, _weights=self._w[b])
+            x = cache_update(x, idx, mask, k, ys, self.xref[b], self.codes[b], self.scale[b],
+                             self.y[b])
+        self.history.append((k, full, delta_t))
+        return x
 
 
 def topk_count(ratio: float, L: int) -> int:

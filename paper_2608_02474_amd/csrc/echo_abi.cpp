@@ -236,6 +236,64 @@ int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref, con
                                      static_cast<hipStream_t>(stream)));
 }
 
+size_t echo_saliency_workspace(const echo_select_cfg* cfg) {
+  if (!select_cfg_ok(cfg)) return 0;
+  const size_t L = static_cast<size_t>(cfg->T) * cfg->N;
+  return 2 * align_up(L * sizeof(double));
+}
+
+int echo_saliency(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
+                  float* saliency, double* step_delta, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!select_cfg_ok(cfg)) return ECHO_EINVAL;
+  if (!ok_ptr(x) || !ok_ptr(xref) || !ok_ptr(frame_weight) || !ok_ptr(saliency)) return ECHO_EINVAL;
+  if (step_delta != nullptr && (reinterpret_cast<uintptr_t>(step_delta) & 7u)) return ECHO_EINVAL;
+  const size_t need = echo_saliency_workspace(cfg);
+  if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
+  const int L = cfg->T * cfg->N;
+  double* num = static_cast<double*>(workspace);
+  double* den = reinterpret_cast<double*>(static_cast<char*>(workspace) + align_up(L * sizeof(double)));
+  return device_status(launch_saliency(cfg->dtype == ECHO_BF16, x, xref, frame_weight, L, cfg->N, cfg->D,
+                                       cfg->xi, saliency, num, den, step_delta,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int echo_topk(const echo_select_cfg* cfg, const float* saliency, int32_t* idx, uint8_t* mask, int32_t* n_sel,
+              void* stream) {
+  if (!select_cfg_ok(cfg)) return ECHO_EINVAL;
+  if (!ok_ptr(saliency) || !ok_ptr(idx) || !ok_ptr(mask) || n_sel == nullptr) return ECHO_EINVAL;
+  const int L = cfg->T * cfg->N;
+  const int threshold_mode = cfg->k < 0 ? 1 : 0;
+  return device_status(launch_topk(saliency, L, threshold_mode ? 0 : cfg->k, threshold_mode, cfg->threshold,
+                                   idx, mask, n_sel, static_cast<hipStream_t>(stream)));
+}
+
+int32_t echo_schedule_next(const echo_schedule_cfg* cfg, echo_schedule_state* st, double delta_t, int32_t L,
+                           int32_t* full) {
+  if (cfg == nullptr || st == nullptr || full == nullptr || L < 1 || cfg->n_full < 0 ||
+      !(cfg->r_min >= 0.0) || !(cfg->r_max <= 1.0) || !(cfg->r_min <= cfg->r_max) || !std::isfinite(cfg->alpha) ||
+      std::isnan(cfg->refresh_delta) || std::isnan(delta_t))
+    return -ECHO_EINVAL;
+  const int32_t step = st->step++;
+  if (step < cfg->n_full) {
+    st->delta_acc = 0.0;
+    *full = 1;
+    return L;
+  }
+  st->delta_acc += delta_t;
+  if (cfg->refresh_delta > 0.0 && st->delta_acc > cfg->refresh_delta) {
+    st->delta_acc = 0.0;
+    *full = 1;
+    return L;
+  }
+  st->delta_max = delta_t > st->delta_max ? delta_t : st->delta_max;
+  const double dhat = st->delta_max > 0.0 ? delta_t / st->delta_max : 0.0;
+  double r = cfg->r_min + cfg->alpha * dhat;
+  r = r < cfg->r_min ? cfg->r_min : (r > cfg->r_max ? cfg->r_max : r);
+  const double kk = std::ceil(r * L - 1e-9);
+  *full = 0;
+  return kk < 0.0 ? 0 : (kk > L ? L : static_cast<int32_t>(kk));
+}
+
 size_t echo_block_workspace(const echo_block_cfg* cfg, int32_t n_sel_max) {
   if (!block_cfg_ok(cfg) || n_sel_max < 0) return 0;
   return block_ws_layout(cfg, n_sel_max, nullptr).bytes;

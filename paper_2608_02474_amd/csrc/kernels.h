@@ -67,6 +67,12 @@ hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const 
                          double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
                          double* step_delta, hipStream_t stream);
 
+hipError_t launch_saliency(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
+                           int D, double xi, float* s, double* num, double* den, double* step_delta,
+                           hipStream_t stream);
+hipError_t launch_topk(const float* s, int L, int k, int threshold_mode, float threshold, int32_t* idx,
+                       uint8_t* mask, int32_t* n_sel, hipStream_t stream);
+
 hipError_t launch_cache_update(int dtype_bf16, const void* x, const int32_t* idx, const uint8_t* mask,
                                int n_sel, int L, int D, const float* y_sel, void* xref, int8_t* codes,
                                float* scale, void* y, hipStream_t stream);

@@ -6,11 +6,11 @@
 //   |x - xref| and |xref| in fp64 (exact per-element differences, so only the
 //   summation order differs from the definition).
 //   Writes s_i = fp32(w_frame * num / (den + xi)) plus num/den for the step sum.
+// step_delta_sum: step-level Eq. 1 sum in a fixed order (deterministic).
 // select_rows: one 1024-thread workgroup, the keys held in registers
-//   (1) step-level Eq. 1 sum in a fixed order (deterministic);
-//   (2) top-K threshold key by 4-pass 8-bit radix select over order-preserving
+//   (1) top-K threshold key by 4-pass 8-bit radix select over order-preserving
 //       uint32 keys (histograms in LDS);
-//   (3) stable compaction in index order: wave ballot + popcount gives each
+//   (2) stable compaction in index order: wave ballot + popcount gives each
 //       lane's rank among equal-key tokens and its output slot; ties at the
 //       threshold key go to the lowest indices.
 // The key set is tiny (4 bytes per token, L2-resident), so one workgroup keeps
@@ -82,6 +82,35 @@ saliency_rows(const T* __restrict__ x, const T* __restrict__ xref, const float* 
   }
 }
 
+// Step-level Eq. 1 value sum(num) / (sum(den) + xi) in a fixed summation
+// order (deterministic): one 1024-thread workgroup.
+__global__ void __launch_bounds__(kSelThreads)
+step_delta_sum(const double* __restrict__ num, const double* __restrict__ den, int L, double xi,
+               double* __restrict__ step_delta) {
+  __shared__ double red_n[kSelWaves], red_d[kSelWaves];
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  double a = 0.0, b = 0.0;
+  for (int i = tid; i < L; i += kSelThreads) {
+    a += num[i];
+    b += den[i];
+  }
+  a = wave_sum(a);
+  b = wave_sum(b);
+  if (lane == 0) {
+    red_n[wave] = a;
+    red_d[wave] = b;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double sa = 0.0, sb = 0.0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      sa += red_n[w];
+      sb += red_d[w];
+    }
+    *step_delta = sa / (sb + xi);
+  }
+}
+
 // Order-preserving key: larger float -> larger key; NaN above everything; -0 == +0.
 __device__ __forceinline__ uint32_t rank_key(float s) {
   if (s != s) return 0xffffffffu;
@@ -96,13 +125,10 @@ __device__ __forceinline__ uint32_t rank_key(float s) {
 template <int R>
 __global__ void __launch_bounds__(kSelThreads)
 select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float threshold,
-            const double* __restrict__ num, const double* __restrict__ den, double xi,
-            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel,
-            double* __restrict__ step_delta) {
+            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sh_digit, sh_above;
   __shared__ uint32_t wcnt[2][kSelWaves];
-  __shared__ double red_n[kSelWaves], red_d[kSelWaves];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const uint64_t lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
 
@@ -123,31 +149,7 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
       return i < L ? rank_key(s[i]) : 0u;
   };
 
-  // (1) step-level relative change, fixed summation order
-  if (step_delta != nullptr) {
-    double a = 0.0, b = 0.0;
-    for (int i = tid; i < L; i += kSelThreads) {
-      a += num[i];
-      b += den[i];
-    }
-    a = wave_sum(a);
-    b = wave_sum(b);
-    if (lane == 0) {
-      red_n[wave] = a;
-      red_d[wave] = b;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      double sa = 0.0, sb = 0.0;
-      for (int w = 0; w < kSelWaves; ++w) {
-        sa += red_n[w];
-        sb += red_d[w];
-      }
-      *step_delta = sa / (sb + xi);
-    }
-  }
-
-  // (2) threshold key and how many tokens equal to it are taken
+  // (1) threshold key and how many tokens equal to it are taken
   uint32_t thr;
   uint32_t need_eq;
   bool take_eq;
@@ -227,7 +229,7 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
     take_eq = true;
   }
 
-  // (3) stable compaction in index order
+  // (2) stable compaction in index order
   uint32_t base_eq = 0, base_sel = 0;
 #pragma unroll
   for (int r = 0; r < (R > 0 ? R : 1); ++r) {
@@ -270,10 +272,9 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
   if (tid == 0) *n_sel = static_cast<int32_t>(base_sel);
 }
 
-hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
-                         int D, double xi, int k, int threshold_mode, float threshold, float* s,
-                         double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
-                         double* step_delta, hipStream_t stream) {
+hipError_t launch_saliency(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
+                           int D, double xi, float* s, double* num, double* den, double* step_delta,
+                           hipStream_t stream) {
   const dim3 grid((L + (kSalThreads / kWave) - 1) / (kSalThreads / kWave));
   const int per_lane = (D / 8 + kWave - 1) / kWave;
   hipError_t e = hipErrorInvalidValue;
@@ -301,17 +302,32 @@ hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const 
   ECHO_SAL_CASE(16)
   ECHO_SAL_CASE(0)
 #undef ECHO_SAL_CASE
-  if (e != hipSuccess) return e;
-#define ECHO_SEL_CASE(RK)                                                                     \
-  if (L <= RK * kSelThreads)                                                                  \
-    return ECHO_LAUNCH("select_rows", select_rows<RK>, dim3(1), dim3(kSelThreads), 0, stream, s, \
-                       L, k, threshold_mode, threshold, num, den, xi, idx, mask, n_sel, step_delta);
+  if (e != hipSuccess || step_delta == nullptr) return e;
+  return ECHO_LAUNCH("step_delta_sum", step_delta_sum, dim3(1), dim3(kSelThreads), 0, stream, num, den, L,
+                     xi, step_delta);
+}
+
+hipError_t launch_topk(const float* s, int L, int k, int threshold_mode, float threshold, int32_t* idx,
+                       uint8_t* mask, int32_t* n_sel, hipStream_t stream) {
+#define ECHO_SEL_CASE(RK)                                                                      \
+  if (L <= RK * kSelThreads)                                                                   \
+    return ECHO_LAUNCH("select_rows", select_rows<RK>, dim3(1), dim3(kSelThreads), 0, stream, s, L, \
+                       k, threshold_mode, threshold, idx, mask, n_sel);
   ECHO_SEL_CASE(8)
   ECHO_SEL_CASE(32)
   ECHO_SEL_CASE(80)
 #undef ECHO_SEL_CASE
   return ECHO_LAUNCH("select_rows", select_rows<0>, dim3(1), dim3(kSelThreads), 0, stream, s, L, k,
-                     threshold_mode, threshold, num, den, xi, idx, mask, n_sel, step_delta);
+                     threshold_mode, threshold, idx, mask, n_sel);
+}
+
+hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
+                         int D, double xi, int k, int threshold_mode, float threshold, float* s,
+                         double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
+                         double* step_delta, hipStream_t stream) {
+  const hipError_t e = launch_saliency(dtype_bf16, x, xref, fw, L, N, D, xi, s, num, den, step_delta, stream);
+  if (e != hipSuccess) return e;
+  return launch_topk(s, L, k, threshold_mode, threshold, idx, mask, n_sel, stream);
 }
 
 }  // namespace echo
