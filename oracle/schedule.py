@@ -24,7 +24,9 @@ Readings:
   whose accumulated Delta since the last full step (its own included)
   exceeds delta is computed in full instead, and the accumulation restarts;
 * one selection per step is shared by every block of the stack: it is taken
-  on the first block's input; block b's input is block b-1's output.
+  on the first block's input; block b's input is block b-1's output;
+* in the two-stage form (anchor segments given) the count is per segment,
+  k_t = ceil(N r_t - 1e-9), with the normalization and the refresh above.
 """
 from __future__ import annotations
 
@@ -69,33 +71,42 @@ def schedule_next(cfg: Schedule, st: ScheduleState, delta_t: float, L: int):
     return k, False
 
 
-def stack_trajectory(blocks, inputs, fw, N, H, cfg: Schedule, dtype: str, xi: float = 1e-6):
+def stack_trajectory(blocks, inputs, fw, N, H, cfg: Schedule, dtype: str, xi: float = 1e-6,
+                     anchors=None, codec: int = 0):
     """Run a stack of cached blocks over a trajectory of first-block inputs.
 
     blocks: list of block parameter dicts; inputs: list of [L, D] first-block
-    inputs, one per denoising step; fw: [T] frame weights.  Returns per step
-    (k, full, delta_t, outputs of the last block)."""
+    inputs, one per denoising step; fw: [T] frame weights.  anchors: None for
+    the global token top-K, else a [T] segment mask for the two-stage
+    selection (k_t = ceil(N r_t) tokens per anchor segment, ranked by
+    saliency with unit frame weights); codec: the cache codec of
+    oracle.variants.  Returns per step (k, full, delta_t, outputs of the last
+    block), k being the schedule's count (per segment in the two-stage form)."""
     from oracle import block as OB
-    from oracle import cache as OC
     from oracle import select as OS
+    from oracle import variants as OV
 
     L, D = inputs[0].shape
-    caches = [OC.empty_cache(L, D) for _ in blocks]
+    caches = [OV.empty_codec_cache(L, D) for _ in blocks]
     st = ScheduleState()
     out = []
     for x0 in inputs:
         x0 = np.asarray(x0, np.float32)
         # Eq. 1 on the first block's input against its cache
-        s, num, den = OS.saliency(x0, caches[0][0], fw, N, xi)
+        w = fw if anchors is None else np.ones(L // N, np.float32)
+        s, num, den = OS.saliency(x0, caches[0][0], w, N, xi)
         delta_t = OS.step_delta(num, den, xi)
-        k, full = schedule_next(cfg, st, delta_t, L)
-        idx = np.arange(L) if full else OS.select_topk(s, k)
+        if anchors is None:
+            k, full = schedule_next(cfg, st, delta_t, L)
+            idx = np.arange(L) if full else OS.select_topk(s, k)
+        else:
+            k, full = schedule_next(cfg, st, delta_t, N)
+            idx = np.arange(L) if full else OV.select_segments(s, anchors, N, k)
         x = x0
-        for p, (i, cache) in zip(blocks, enumerate(caches)):
-            y_sel = (OB.block_partial(p, x, idx, H).astype(np.float32) if k
+        for i, p in enumerate(blocks):
+            y_sel = (OB.block_partial(p, x, idx, H).astype(np.float32) if len(idx)
                      else np.zeros((0, D), np.float32))
-            y, xref, codes, scale = OC.cache_update(x, idx, y_sel, *cache, dtype)
-            caches[i] = (xref, codes, scale)
+            y, *caches[i] = OV.cache_update_codec(codec, x, idx, y_sel, *caches[i], dtype)
             x = y
         out.append((k, full, delta_t, x))
     return out

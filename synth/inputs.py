@@ -222,3 +222,9 @@ def random_frame_weight(T: int, seed: int) -> np.ndarray:
     """Arbitrary per-frame weights in [0, 1] (for selection tests that do not
     go through the audio path)."""
     return _rng(seed, 99).uniform(0.0, 1.0, size=T).astype(np.float32)
+
+
+def random_anchor_keys(T: int, seed: int) -> np.ndarray:
+    """Uniform [0, 1) keys, one per segment: the random draw behind the Random
+    anchor strategy (its k anchors are the k largest keys)."""
+    return _rng(seed, 98).uniform(0.0, 1.0, size=T).astype(np.float32)
