@@ -141,6 +141,38 @@ int echo_saliency(const echo_select_cfg* cfg, const void* x, const void* xref,
 int echo_topk(const echo_select_cfg* cfg, const float* saliency, int32_t* idx, uint8_t* mask,
               int32_t* n_sel, void* stream);
 
+/* ------------------------------------------------ two-stage selection */
+/*
+ * The literal form of the saliency anchors (Sec. 3.3, "Cross-modal Saliency
+ * Anchors": top-k segments of the audio energy before generation; "Energy-
+ * Guided Step-Latent Cache Scheduling": k_t = ceil(N r_t) latents per selected
+ * segment) and the anchor strategies of the module ablation (Table 2:
+ * Uniform, Random).
+ *
+ * echo_anchors writes anchors[T] (uint8 0/1):
+ *   ECHO_ANCHOR_TOPK     the k segments ranked first by (keys desc, index asc),
+ *                        NaN first.  keys [T] fp32: the frame energies of
+ *                        echo_energy for the energy anchors, uniform random
+ *                        numbers drawn by the caller for Random anchors;
+ *   ECHO_ANCHOR_UNIFORM  the evenly spaced segments floor((2j + 1) T / (2k)),
+ *                        j = 0..k-1 (keys unused, may be NULL).
+ * Requires 1 <= T <= 4096, 0 <= k <= T.  One workgroup, O(T^2 / 1024) work.
+ *
+ * echo_topk_segments selects, in every anchor segment t (tokens [tN, tN + N)),
+ * the min(k, N) tokens ranked first by (saliency desc, index asc), NaN first,
+ * with the ranking rules of echo_topk; other segments' tokens are unselected.
+ * Writes idx[0 .. n) ascending (n = number of anchors * min(k, N); idx must
+ * hold that many, L always suffices), mask[L] (their indicator) and *n_sel = n
+ * (device int32).  Give it the saliency of echo_saliency with unit frame
+ * weights: a positive weight per segment cannot change the order inside one.
+ * Requires 1 <= T <= 65535, N >= 1, T*N < 2^31, k >= 0.
+ */
+typedef enum { ECHO_ANCHOR_TOPK = 0, ECHO_ANCHOR_UNIFORM = 1 } echo_anchor_mode;
+
+int echo_anchors(const float* keys, int32_t T, int32_t k, int32_t mode, uint8_t* anchors, void* stream);
+int echo_topk_segments(const float* saliency, const uint8_t* anchors, int32_t T, int32_t N, int32_t k,
+                       int32_t* idx, uint8_t* mask, int32_t* n_sel, void* stream);
+
 /* ---------------------------------------------------------- step schedule */
 /*
  * Step-level cache schedule (Sec. 3.3, "Energy-Guided Step-Latent Cache
@@ -252,6 +284,31 @@ typedef struct {
 int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* idx,
                       const uint8_t* mask, int32_t n_sel, const float* y_sel,
                       void* xref, int8_t* codes, float* scale, void* y, void* stream);
+
+/*
+ * The cache codecs of the module ablation (Table 2: "FP16" and "Naive INT8"
+ * against the residual int8 cache), with echo_cache_update's fusion:
+ *   ECHO_CODEC_RESIDUAL_INT8  exactly echo_cache_update (store unused, may be NULL);
+ *   ECHO_CODEC_FULL           a selected row stores cast(y_sel[j]) into store_i;
+ *                             an unselected row outputs store_i unchanged
+ *                             (store [L][D] `dtype`; codes and scale unused,
+ *                             may be NULL);
+ *   ECHO_CODEC_NAIVE_INT8     a selected row is quantized itself: amax = max|y_sel[j]|,
+ *                             scale and codes as above with res = y_sel[j];
+ *                             an unselected row outputs cast(fp32(scale_i * code))
+ *                             (store unused, may be NULL).
+ * Every codec sets xref_i = x_i and y_i = cast(y_sel[j]) for a selected row.
+ * Requirements as for echo_cache_update.
+ */
+typedef enum {
+  ECHO_CODEC_RESIDUAL_INT8 = 0,
+  ECHO_CODEC_FULL = 1,
+  ECHO_CODEC_NAIVE_INT8 = 2
+} echo_codec;
+
+int echo_cache_update_codec(const echo_cache_cfg* cfg, int32_t codec, const void* x, const int32_t* idx,
+                            const uint8_t* mask, int32_t n_sel, const float* y_sel, void* xref, void* store,
+                            int8_t* codes, float* scale, void* y, void* stream);
 
 /* ---------------------------------------------- adaptive reference cache */
 /*

@@ -16,6 +16,8 @@ HEADER = os.path.join(HERE, "..", "include", "echo.h")
 ECHO_OK, ECHO_EINVAL, ECHO_EUNSUPPORTED, ECHO_EWORKSPACE, ECHO_EDEVICE = range(5)
 ECHO_F32, ECHO_BF16 = 0, 1
 ECHO_BLOCK_BATCH_INVARIANT = 1
+ECHO_ANCHOR_TOPK, ECHO_ANCHOR_UNIFORM = 0, 1
+ECHO_CODEC_RESIDUAL_INT8, ECHO_CODEC_FULL, ECHO_CODEC_NAIVE_INT8 = 0, 1, 2
 
 c_int32, c_int64, c_size_t, c_void_p, c_float, c_double = (
     ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float,
@@ -85,6 +87,9 @@ _SIGNATURES = {
     "echo_saliency": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p,
                                      c_void_p, c_void_p, c_size_t, c_void_p]),
     "echo_topk": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+    "echo_anchors": (ctypes.c_int, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
+    "echo_topk_segments": (ctypes.c_int, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
+                                          c_void_p, c_void_p, c_void_p]),
     "echo_schedule_next": (c_int32, [_P(ScheduleCfg), _P(ScheduleState), c_double, c_int32,
                                      _P(c_int32)]),
     "echo_block_workspace": (c_size_t, [_P(BlockCfg), c_int32]),
@@ -93,6 +98,9 @@ _SIGNATURES = {
     "echo_cache_update": (ctypes.c_int, [_P(CacheCfg), c_void_p, c_void_p, c_void_p, c_int32,
                                          c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                          c_void_p]),
+    "echo_cache_update_codec": (ctypes.c_int, [_P(CacheCfg), c_int32, c_void_p, c_void_p, c_void_p,
+                                               c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                               c_void_p, c_void_p, c_void_p]),
     "echo_refcache_init": (ctypes.c_int, [_P(RefCacheCfg), _P(RefCacheState), c_void_p]),
     "echo_refcache_update": (ctypes.c_int, [_P(RefCacheCfg), _P(RefCacheState), c_void_p,
                                             c_void_p, c_void_p, c_int32, c_void_p, c_void_p,

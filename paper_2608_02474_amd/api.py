@@ -203,8 +203,62 @@ def topk(sel: Selection, N: int, D: int, dtype, k: int | None = None,
     return sel
 
 
+ANCHOR_MODES = ("energy", "uniform", "random")
+
+
+def anchors(T: int, k: int, mode: str = "energy", keys: torch.Tensor | None = None,
+            out: torch.Tensor | None = None, device=None) -> torch.Tensor:
+    """Anchor segments, uint8 [T] on the device (echo_anchors): "energy" and
+    "random" take the k segments with the largest keys (the frame energies,
+    or per-clip uniform random numbers the caller draws); "uniform" the
+    evenly spaced ones (keys unused)."""
+    lib = _lib_handle()
+    if mode not in ANCHOR_MODES:
+        raise ValueError(f"mode must be one of {ANCHOR_MODES}")
+    if mode == "uniform":
+        dev = keys.device if keys is not None else device
+        kp = None
+    else:
+        if keys is None:
+            raise ValueError(f"{mode} anchors need keys")
+        _dev(keys, "keys", torch.float32)
+        dev, kp = keys.device, _ptr(keys)
+    if out is None:
+        out = torch.empty(T, dtype=torch.uint8, device=dev)
+    m = _lib.ECHO_ANCHOR_UNIFORM if mode == "uniform" else _lib.ECHO_ANCHOR_TOPK
+    check("echo_anchors", lib.echo_anchors(kp, int(T), int(k), m, _ptr(out), _stream()))
+    return out
+
+
+def topk_segments(sel: Selection, anchor_mask: torch.Tensor, N: int, k: int) -> Selection:
+    """Two-stage selection from sel.saliency: min(k, N) tokens in every anchor
+    segment into sel.idx / sel.mask / sel.n_sel_dev (echo_topk_segments)."""
+    lib = _lib_handle()
+    L = sel.saliency.numel()
+    T = anchor_mask.numel()
+    if T * N != L:
+        raise ValueError("anchor mask and saliency disagree on T * N")
+    _dev(anchor_mask, "anchors", torch.uint8)
+    check("echo_topk_segments",
+          lib.echo_topk_segments(_ptr(sel.saliency), _ptr(anchor_mask), T, int(N), int(k), _ptr(sel.idx),
+                                 _ptr(sel.mask), _ptr(sel.n_sel_dev), _stream()))
+    sel.n_sel = None
+    return sel
+
+
 class Scheduler:
     """Step-level cache schedule (echo_schedule_next, a host function)."""
+
+    @classmethod
+    def step_only(cls, n_full: int, refresh_delta: float) -> "Scheduler":
+        """Whole-step caching: cached steps recompute nothing; the Eq. 2
+        refresh recomputes whole steps."""
+        return cls(n_full, 0.0, 0.0, 0.0, refresh_delta)
+
+    @classmethod
+    def latent_only(cls, n_full: int, ratio: float) -> "Scheduler":
+        """A fixed token ratio on every cached step."""
+        return cls(n_full, ratio, ratio, 0.0)
 
     def __init__(self, n_full: int, r_min: float, r_max: float, alpha: float,
                  refresh_delta: float = 0.0):
@@ -225,44 +279,79 @@ class Scheduler:
 class BlockStack:
     """A stack of cached blocks over a denoising trajectory: per step one Eq. 1
     value and one selection on the first block's input (shared by all blocks),
-    the scheduled K, then block_partial + cache_update block after block."""
+    the scheduled K, then block_partial + the cache update block after block.
+
+    anchor_mask (uint8 [T] on the device, from `anchors`) switches to the
+    two-stage selection: k_t = ceil(N r_t) tokens per anchor segment, ranked
+    by the saliency with unit frame weights.  codec: "residual_int8" (the
+    default), "full" (the outputs in the activation dtype) or "naive_int8"."""
+
+    CODECS = {"residual_int8": 0, "full": 1, "naive_int8": 2}
 
     def __init__(self, params: list, H: int, L: int, D: int, device, dtype, scheduler: Scheduler,
-                 xi: float = 1e-6, ln_eps: float = 1e-6):
+                 xi: float = 1e-6, ln_eps: float = 1e-6, anchor_mask: torch.Tensor | None = None,
+                 codec: str = "residual_int8"):
         if scheduler.cfg.n_full < 1:
             raise ValueError("the first step must be a full step (n_full >= 1)")
+        if codec not in self.CODECS:
+            raise ValueError(f"codec must be one of {tuple(self.CODECS)}")
         self.params, self.H, self.L, self.D = params, H, L, D
         self.sched, self.xi, self.ln_eps = scheduler, xi, ln_eps
+        self.anchor_mask, self.codec = anchor_mask, self.CODECS[codec]
         kw = dict(device=device)
+        full = self.codec == self.CODECS["full"]
         self.xref = [torch.zeros((L, D), dtype=dtype, **kw) for _ in params]
-        self.codes = [torch.zeros((L, D), dtype=torch.int8, **kw) for _ in params]
-        self.scale = [torch.zeros(L, dtype=torch.float32, **kw) for _ in params]
+        self.codes = [None if full else torch.zeros((L, D), dtype=torch.int8, **kw) for _ in params]
+        self.scale = [None if full else torch.zeros(L, dtype=torch.float32, **kw) for _ in params]
+        self.store = [torch.zeros((L, D), dtype=dtype, **kw) if full else None for _ in params]
         self.y = [torch.empty((L, D), dtype=dtype, **kw) for _ in params]
         self.y_sel = torch.empty((L, D), dtype=torch.float32, **kw)
         self.all_idx = torch.arange(L, dtype=torch.int32, **kw)
         self.all_mask = torch.ones(L, dtype=torch.uint8, **kw)
         self._w = [block_weights(p) for p in params]
         self.ws, self.sel_ws, self.sel = Workspace(), Workspace(), None
-        self.history = []   # (k, full, delta_t) per step
+        self._unit, self._anchor_count = None, None
+        self.history = []   # (k, full, delta_t) per step; k per segment in the two-stage form
 
     def step(self, x0: torch.Tensor, frame_weight: torch.Tensor, N: int) -> torch.Tensor:
+        two_stage = self.anchor_mask is not None
+        if two_stage:
+            if self._unit is None or self._unit.numel() != self.L // N:
+                self._unit = torch.ones(self.L // N, dtype=torch.float32, device=x0.device)
+            frame_weight = self._unit
         self.sel = saliency(x0, self.xref[0], frame_weight, N, self.xi, out=self.sel,
                             workspace=self.sel_ws)
         delta_t = float(self.sel.step_delta[0].item())      # host needs it to choose K
-        k, full = self.sched.next(delta_t, self.L)
+        k, full = self.sched.next(delta_t, N if two_stage else self.L)
         if full:
-            idx, mask, k = self.all_idx, self.all_mask, self.L
+            idx, mask, n = self.all_idx, self.all_mask, self.L
+        elif two_stage:
+            # the count is fixed by k and the anchors: no device read-back
+            topk_segments(self.sel, self.anchor_mask, N, k)
+            idx, mask, n = self.sel.idx, self.sel.mask, self._n_anchor * min(k, N)
         else:
             topk(self.sel, N, self.D, x0.dtype, k=k)
-            idx, mask = self.sel.idx, self.sel.mask
+            idx, mask, n = self.sel.idx, self.sel.mask, k
         x = x0
         for b, p in enumerate(self.params):
-            ys = block_partial(p, x, idx, k, self.H, self.ln_eps, y_sel=self.y_sel,
+            ys = block_partial(p, x, idx, n, self.H, self.ln_eps, y_sel=self.y_sel,
                                workspace=self.ws, _weights=self._w[b])
-            x = cache_update(x, idx, mask, k, ys, self.xref[b], self.codes[b], self.scale[b],
-                             self.y[b])
+            x = cache_update_codec(self.codec, x, idx, mask, n, ys, self.xref[b], self.y[b],
+                                   store=self.store[b], codes=self.codes[b], scale=self.scale[b])
         self.history.append((k, full, delta_t))
         return x
+
+    @property
+    def _n_anchor(self) -> int:
+        if self._anchor_count is None:
+            self._anchor_count = int(self.anchor_mask.sum().item())   # once per clip
+        return self._anchor_count
+
+    def cache_bytes(self) -> int:
+        """Device bytes of the per-block cache state (saliency reference,
+        codes and scales or the 16-bit store)."""
+        t = [*self.xref, *self.codes, *self.scale, *self.store]
+        return sum(a.numel() * a.element_size() for a in t if a is not None)
 
 
 def topk_count(ratio: float, L: int) -> int:
@@ -337,6 +426,36 @@ def cache_update(x: torch.Tensor, idx: torch.Tensor, mask: torch.Tensor, n_sel: 
           lib.echo_cache_update(ctypes.byref(cfg), _ptr(x), _ptr(idx) if n_sel else None,
                                 _ptr(mask), n_sel, _ptr(y_sel) if n_sel else None, _ptr(xref),
                                 _ptr(codes), _ptr(scale), _ptr(y), _stream()))
+    return y
+
+
+def cache_update_codec(codec: int, x: torch.Tensor, idx: torch.Tensor, mask: torch.Tensor, n_sel: int,
+                       y_sel: torch.Tensor, xref: torch.Tensor, y: torch.Tensor | None = None,
+                       store: torch.Tensor | None = None, codes: torch.Tensor | None = None,
+                       scale: torch.Tensor | None = None) -> torch.Tensor:
+    """echo_cache_update_codec: codec 0 residual int8 (codes, scale), 1 the
+    output in the activation dtype (store), 2 int8 of the output itself
+    (codes, scale).  Updates the cache state in place; returns y."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    L, D = x.shape
+    _dev(mask, "mask", torch.uint8)
+    _dev(xref, "xref", x.dtype)
+    if codec == _lib.ECHO_CODEC_FULL:
+        _dev(store, "store", x.dtype)
+    else:
+        _dev(codes, "codes", torch.int8)
+        _dev(scale, "scale", torch.float32)
+    if n_sel > 0:
+        _dev(idx, "idx", torch.int32)
+        _dev(y_sel, "y_sel", torch.float32)
+    if y is None:
+        y = torch.empty_like(x)
+    cfg = CacheCfg(L, D, _echo_dtype(x))
+    check("echo_cache_update_codec",
+          lib.echo_cache_update_codec(ctypes.byref(cfg), int(codec), _ptr(x), _ptr(idx) if n_sel else None,
+                                      _ptr(mask), n_sel, _ptr(y_sel) if n_sel else None, _ptr(xref),
+                                      _ptr(store), _ptr(codes), _ptr(scale), _ptr(y), _stream()))
     return y
 
 

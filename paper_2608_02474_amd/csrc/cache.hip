@@ -14,6 +14,14 @@
 // Every fp32 step is a separately rounded IEEE operation (no fused
 // multiply-add), so codes and reused rows are exactly the fp32 values the
 // definition gives.
+//
+// Codecs of the module ablation (Table 2), one template parameter:
+//   kResidualInt8  the cache above (reference x_i, int8 residual y - x_i);
+//   kFull          the output itself in the activation dtype: a fresh row
+//                  also goes to `store`, a reused row is copied from it;
+//   kNaiveInt8     int8 codes of y itself (no reference), read back as
+//                  cast(fp32(scale * code)).
+// Every codec records xref_i := x_i for a fresh row (the saliency reference).
 #include <type_traits>
 
 #include "common.h"
@@ -24,6 +32,7 @@ namespace echo {
 
 constexpr int kCacheThreads = 256;
 constexpr int kCacheWavesPerBlock = kCacheThreads / kWave;
+constexpr int kResidualInt8 = 0, kFull = 1, kNaiveInt8 = 2;
 
 __device__ __forceinline__ void load8(const float* p, float* v) {
   const uint4 a = ldg16(p), b = ldg16(p + 4);
@@ -67,12 +76,16 @@ __device__ __forceinline__ void quantize8(const float* res, float inv, int8_t* d
 
 // MAXC > 0: the fresh row's residual stays in registers (D <= 512 * MAXC);
 // MAXC == 0: the row is streamed twice (any D).
-template <typename T, int MAXC>
+template <typename T, int MAXC, int CODEC>
 __global__ void __launch_bounds__(kCacheThreads)
 cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
                   const uint8_t* __restrict__ mask, int n_sel, int L, int D,
-                  const float* __restrict__ y_sel, T* __restrict__ xref, int8_t* __restrict__ codes,
-                  float* __restrict__ scale, T* __restrict__ y) {
+                  const float* __restrict__ y_sel, T* __restrict__ xref, T* __restrict__ store,
+                  int8_t* __restrict__ codes, float* __restrict__ scale, T* __restrict__ y) {
+  // the value a fresh element is quantized from: its residual or itself
+  auto qsrc = [](float yv, float xv) __attribute__((always_inline)) {
+    return CODEC == kNaiveInt8 ? yv : __fsub_rn(yv, xv);
+  };
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t g = static_cast<int64_t>(blockIdx.x) * kCacheWavesPerBlock + wave;
   const int nch = D / 8;
@@ -105,8 +118,12 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
             xraw[u].unpack(xv);
             store8(y + i * D + c * 8, yv);      // fresh output, cast to storage type
             xraw[u].store(xref + i * D + c * 8);  // reference := current input
+            if constexpr (CODEC == kFull) {
+              store8(store + i * D + c * 8, yv);
+            } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(__fsub_rn(yv[j], xv[j])));
+              for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(qsrc(yv[j], xv[j])));
+            }
           }
         }
       };
@@ -114,15 +131,24 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
         body(std::integral_constant<bool, true>{});
       else
         body(std::integral_constant<bool, false>{});
+    } else if constexpr (CODEC == kFull) {
+      for (int c = lane; c < nch; c += kWave) {
+        float yv[8];
+        load8(ys + c * 8, yv);
+        store8(y + i * D + c * 8, yv);
+        store8(store + i * D + c * 8, yv);
+        copy8(xi + c * 8, xref + i * D + c * 8);
+      }
     } else {
       for (int c = lane; c < nch; c += kWave) {
         float yv[8], xv[8];
         load8(ys + c * 8, yv);
         load8(xi + c * 8, xv);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(__fsub_rn(yv[j], xv[j])));
+        for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(qsrc(yv[j], xv[j])));
       }
     }
+    if constexpr (CODEC == kFull) return;
     amax = wave_max(amax);
     const bool nz = amax > 0.0f;
     const float inv = nz ? __fdiv_rn(127.0f, amax) : 0.0f;
@@ -136,7 +162,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
           yraw[u].unpack(yv);
           xraw[u].unpack(xv);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) r[j] = __fsub_rn(yv[j], xv[j]);  // the same residual as above
+          for (int j = 0; j < 8; ++j) r[j] = qsrc(yv[j], xv[j]);  // the same values as above
           quantize8(r, inv, codes + i * D + c * 8);
         }
       }
@@ -146,7 +172,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
         load8(ys + c * 8, yv);
         load8(xi + c * 8, xv);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) r[j] = __fsub_rn(yv[j], xv[j]);
+        for (int j = 0; j < 8; ++j) r[j] = qsrc(yv[j], xv[j]);
         quantize8(r, inv, codes + i * D + c * 8);
         store8(y + i * D + c * 8, yv);
         copy8(xi + c * 8, xref + i * D + c * 8);
@@ -156,6 +182,25 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
   }
   const int64_t i = g - n_sel;
   if (i >= L || mask[i]) return;
+  if constexpr (CODEC == kFull) {
+    if (MAXC > 0) {
+      constexpr int R = MAXC > 0 ? MAXC : 1;
+      Raw8<T> rr[R];
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        if (c < nch) rr[u].load(store + i * D + c * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int c = lane + u * kWave;
+        if (c < nch) rr[u].store(y + i * D + c * 8);
+      }
+    } else {
+      for (int c = lane; c < nch; c += kWave) copy8(store + i * D + c * 8, y + i * D + c * 8);
+    }
+    return;
+  }
   const float sc = scale[i];
   auto reuse8 = [&](const Raw8<T>& rr, uint2 cw, int c) __attribute__((always_inline)) {
     float r[8], out[8];
@@ -164,7 +209,8 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int8_t q = static_cast<int8_t>((w[j / 4] >> (8 * (j % 4))) & 0xffu);
-      out[j] = mul_add_unfused(sc, static_cast<float>(q), r[j]);
+      out[j] = CODEC == kNaiveInt8 ? __fmul_rn(sc, static_cast<float>(q))
+                                   : mul_add_unfused(sc, static_cast<float>(q), r[j]);
     }
     store8(y + i * D + c * 8, out);
   };
@@ -178,7 +224,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
       for (int u = 0; u < R; ++u) {
         const int c = lane + u * kWave;
         const int cc = FULL || c < nch ? c : nch - 1;
-        rr[u].load(xref + i * D + cc * 8);
+        if constexpr (CODEC != kNaiveInt8) rr[u].load(xref + i * D + cc * 8);
         cw[u] = *reinterpret_cast<const uint2*>(codes + i * D + cc * 8);
       }
 #pragma unroll
@@ -194,23 +240,23 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
   } else {
     for (int c = lane; c < nch; c += kWave) {
       Raw8<T> rr;
-      rr.load(xref + i * D + c * 8);
+      if constexpr (CODEC != kNaiveInt8) rr.load(xref + i * D + c * 8);
       reuse8(rr, *reinterpret_cast<const uint2*>(codes + i * D + c * 8), c);
     }
   }
 }
 
-template <typename T>
+template <typename T, int CODEC>
 static hipError_t launch_cache_t(const char* name, const T* x, const int32_t* idx, const uint8_t* mask,
-                                 int n_sel, int L, int D, const float* y_sel, T* xref, int8_t* codes,
-                                 float* scale, T* y, hipStream_t stream) {
+                                 int n_sel, int L, int D, const float* y_sel, T* xref, T* store,
+                                 int8_t* codes, float* scale, T* y, hipStream_t stream) {
   const int64_t waves = static_cast<int64_t>(n_sel) + L;
   const dim3 grid(static_cast<unsigned>((waves + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
   const int per_lane = (D / 8 + kWave - 1) / kWave;
-#define ECHO_CACHE_CASE(MC)                                                                    \
-  if (per_lane <= MC)                                                                          \
-    return ECHO_LAUNCH(name, (cache_update_rows<T, MC>), grid, dim3(kCacheThreads), 0, stream, \
-                       x, idx, mask, n_sel, L, D, y_sel, xref, codes, scale, y);
+#define ECHO_CACHE_CASE(MC)                                                                           \
+  if (per_lane <= MC)                                                                                 \
+    return ECHO_LAUNCH(name, (cache_update_rows<T, MC, CODEC>), grid, dim3(kCacheThreads), 0, stream, \
+                       x, idx, mask, n_sel, L, D, y_sel, xref, store, codes, scale, y);
   ECHO_CACHE_CASE(1)
   ECHO_CACHE_CASE(2)
   ECHO_CACHE_CASE(3)
@@ -221,20 +267,47 @@ static hipError_t launch_cache_t(const char* name, const T* x, const int32_t* id
   ECHO_CACHE_CASE(12)
   ECHO_CACHE_CASE(16)
 #undef ECHO_CACHE_CASE
-  return ECHO_LAUNCH(name, (cache_update_rows<T, 0>), grid, dim3(kCacheThreads), 0, stream, x, idx,
-                     mask, n_sel, L, D, y_sel, xref, codes, scale, y);
+  return ECHO_LAUNCH(name, (cache_update_rows<T, 0, CODEC>), grid, dim3(kCacheThreads), 0, stream, x, idx,
+                     mask, n_sel, L, D, y_sel, xref, store, codes, scale, y);
+}
+
+template <typename T>
+static hipError_t launch_codec(int codec, const T* x, const int32_t* idx, const uint8_t* mask, int n_sel,
+                               int L, int D, const float* y_sel, T* xref, T* store, int8_t* codes,
+                               float* scale, T* y, hipStream_t stream) {
+  constexpr bool B = sizeof(T) == 2;
+  switch (codec) {
+    case kResidualInt8:
+      return launch_cache_t<T, kResidualInt8>(B ? "cache_update_bf16" : "cache_update_f32", x, idx, mask,
+                                              n_sel, L, D, y_sel, xref, store, codes, scale, y, stream);
+    case kFull:
+      return launch_cache_t<T, kFull>(B ? "cache_update_full_bf16" : "cache_update_full_f32", x, idx, mask,
+                                      n_sel, L, D, y_sel, xref, store, codes, scale, y, stream);
+    case kNaiveInt8:
+      return launch_cache_t<T, kNaiveInt8>(B ? "cache_update_naive_bf16" : "cache_update_naive_f32", x, idx,
+                                           mask, n_sel, L, D, y_sel, xref, store, codes, scale, y, stream);
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_cache_codec(int dtype_bf16, int codec, const void* x, const int32_t* idx,
+                              const uint8_t* mask, int n_sel, int L, int D, const float* y_sel, void* xref,
+                              void* store, int8_t* codes, float* scale, void* y, hipStream_t stream) {
+  if (dtype_bf16)
+    return launch_codec<bf16_t>(codec, static_cast<const bf16_t*>(x), idx, mask, n_sel, L, D, y_sel,
+                                static_cast<bf16_t*>(xref), static_cast<bf16_t*>(store), codes, scale,
+                                static_cast<bf16_t*>(y), stream);
+  return launch_codec<float>(codec, static_cast<const float*>(x), idx, mask, n_sel, L, D, y_sel,
+                             static_cast<float*>(xref), static_cast<float*>(store), codes, scale,
+                             static_cast<float*>(y), stream);
 }
 
 hipError_t launch_cache_update(int dtype_bf16, const void* x, const int32_t* idx, const uint8_t* mask,
                                int n_sel, int L, int D, const float* y_sel, void* xref, int8_t* codes,
                                float* scale, void* y, hipStream_t stream) {
-  if (dtype_bf16)
-    return launch_cache_t<bf16_t>("cache_update_bf16", static_cast<const bf16_t*>(x), idx, mask, n_sel,
-                                  L, D, y_sel, static_cast<bf16_t*>(xref), codes, scale,
-                                  static_cast<bf16_t*>(y), stream);
-  return launch_cache_t<float>("cache_update_f32", static_cast<const float*>(x), idx, mask, n_sel, L,
-                               D, y_sel, static_cast<float*>(xref), codes, scale,
-                               static_cast<float*>(y), stream);
+  return launch_cache_codec(dtype_bf16, kResidualInt8, x, idx, mask, n_sel, L, D, y_sel, xref, nullptr, codes,
+                            scale, y, stream);
 }
 
 }  // namespace echo

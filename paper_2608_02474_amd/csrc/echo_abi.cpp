@@ -267,6 +267,23 @@ int echo_topk(const echo_select_cfg* cfg, const float* saliency, int32_t* idx, u
                                    idx, mask, n_sel, static_cast<hipStream_t>(stream)));
 }
 
+int echo_anchors(const float* keys, int32_t T, int32_t k, int32_t mode, uint8_t* anchors, void* stream) {
+  if (T < 1 || T > max_anchor_segments() || k < 0 || k > T) return ECHO_EINVAL;
+  if (mode != ECHO_ANCHOR_TOPK && mode != ECHO_ANCHOR_UNIFORM) return ECHO_EINVAL;
+  if (anchors == nullptr || (mode == ECHO_ANCHOR_TOPK && !ok_ptr(keys))) return ECHO_EINVAL;
+  return device_status(launch_anchors(keys, T, k, mode, anchors, static_cast<hipStream_t>(stream)));
+}
+
+int echo_topk_segments(const float* saliency, const uint8_t* anchors, int32_t T, int32_t N, int32_t k,
+                       int32_t* idx, uint8_t* mask, int32_t* n_sel, void* stream) {
+  if (T < 1 || T > 65535 || N < 1 || k < 0) return ECHO_EINVAL;
+  if (static_cast<int64_t>(T) * N >= (int64_t(1) << 31)) return ECHO_EINVAL;
+  if (!ok_ptr(saliency) || anchors == nullptr || !ok_ptr(idx) || !ok_ptr(mask) || n_sel == nullptr)
+    return ECHO_EINVAL;
+  return device_status(
+      launch_topk_segments(saliency, anchors, T, N, k, idx, mask, n_sel, static_cast<hipStream_t>(stream)));
+}
+
 int32_t echo_schedule_next(const echo_schedule_cfg* cfg, echo_schedule_state* st, double delta_t, int32_t L,
                            int32_t* full) {
   if (cfg == nullptr || st == nullptr || full == nullptr || L < 1 || cfg->n_full < 0 ||
@@ -408,6 +425,22 @@ int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* i
   return device_status(launch_cache_update(cfg->dtype == ECHO_BF16, x, idx, mask, n_sel, cfg->L, cfg->D,
                                            y_sel, xref, codes, scale, y,
                                            static_cast<hipStream_t>(stream)));
+}
+
+int echo_cache_update_codec(const echo_cache_cfg* cfg, int32_t codec, const void* x, const int32_t* idx,
+                            const uint8_t* mask, int32_t n_sel, const float* y_sel, void* xref, void* store,
+                            int8_t* codes, float* scale, void* y, void* stream) {
+  if (cfg == nullptr || cfg->L < 1 || cfg->D < 8 || (cfg->D % 8) != 0 || cfg->D > 16384 ||
+      !ok_dtype(cfg->dtype))
+    return ECHO_EINVAL;
+  if (codec != ECHO_CODEC_RESIDUAL_INT8 && codec != ECHO_CODEC_FULL && codec != ECHO_CODEC_NAIVE_INT8)
+    return ECHO_EINVAL;
+  if (n_sel < 0 || n_sel > cfg->L) return ECHO_EINVAL;
+  if (!ok_ptr(x) || !ok_ptr(mask) || !ok_ptr(xref) || !ok_ptr(y)) return ECHO_EINVAL;
+  if (codec == ECHO_CODEC_FULL ? !ok_ptr(store) : (!ok_ptr(codes) || !ok_ptr(scale))) return ECHO_EINVAL;
+  if (n_sel > 0 && (!ok_ptr(idx) || !ok_ptr(y_sel))) return ECHO_EINVAL;
+  return device_status(launch_cache_codec(cfg->dtype == ECHO_BF16, codec, x, idx, mask, n_sel, cfg->L, cfg->D,
+                                          y_sel, xref, store, codes, scale, y, static_cast<hipStream_t>(stream)));
 }
 
 namespace {

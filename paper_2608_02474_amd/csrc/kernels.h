@@ -73,9 +73,22 @@ hipError_t launch_saliency(int dtype_bf16, const void* x, const void* xref, cons
 hipError_t launch_topk(const float* s, int L, int k, int threshold_mode, float threshold, int32_t* idx,
                        uint8_t* mask, int32_t* n_sel, hipStream_t stream);
 
+// two-stage selection (anchor segments, then min(k, N) tokens per anchor)
+hipError_t launch_topk_segments(const float* s, const uint8_t* anchors, int T, int N, int k, int32_t* idx,
+                                uint8_t* mask, int32_t* n_sel, hipStream_t stream);
+// anchor segments: mode 0 top-k of keys, mode 1 evenly spaced; T <= max_anchor_segments()
+hipError_t launch_anchors(const float* keys, int T, int k, int mode, uint8_t* anchors, hipStream_t stream);
+int max_anchor_segments();
+
 hipError_t launch_cache_update(int dtype_bf16, const void* x, const int32_t* idx, const uint8_t* mask,
                                int n_sel, int L, int D, const float* y_sel, void* xref, int8_t* codes,
                                float* scale, void* y, hipStream_t stream);
+
+// codec 0: int8 residual against xref (launch_cache_update); 1: the output in
+// the activation dtype in `store`; 2: int8 codes of the output itself
+hipError_t launch_cache_codec(int dtype_bf16, int codec, const void* x, const int32_t* idx,
+                              const uint8_t* mask, int n_sel, int L, int D, const float* y_sel, void* xref,
+                              void* store, int8_t* codes, float* scale, void* y, hipStream_t stream);
 
 hipError_t launch_refcache_init(int L, int n_chains, int capacity, int32_t* refcount, int32_t* free_list,
                                 int32_t* free_top, int32_t* chain_ref, int32_t* ent_slot, uint8_t* ent_kind,

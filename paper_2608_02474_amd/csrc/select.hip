@@ -15,6 +15,10 @@
 //       threshold key go to the lowest indices.
 // The key set is tiny (4 bytes per token, L2-resident), so one workgroup keeps
 // the selection exact and deterministic at a cost of a few microseconds.
+// select_segments: the same selection per anchor segment, one workgroup per
+//   segment (the two-stage form: anchor segments, then min(k, N) tokens each).
+// anchor_select: the anchor segments (top-k of per-segment keys, or evenly
+//   spaced), one workgroup.
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
@@ -119,13 +123,16 @@ __device__ __forceinline__ uint32_t rank_key(float s) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Top-k (or threshold) selection of L keys by one 1024-thread workgroup:
+// writes mask[0..L), the selected positions i as idx_base + i in ascending
+// order to idx[0..), and their number to *n_sel if n_sel is not null.
 // R > 0: the L keys are loaded once into registers (key r*1024 + tid in
 // slot r, L <= 1024 R), all loads in flight together; every later pass works
 // on the registers.  R == 0: keys are re-read from s on every pass (any L).
 template <int R>
-__global__ void __launch_bounds__(kSelThreads)
-select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float threshold,
-            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
+__device__ __forceinline__ void topk_rows(const float* __restrict__ s, int L, int k, int threshold_mode,
+                                          float threshold, int idx_base, int32_t* __restrict__ idx,
+                                          uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sh_digit, sh_above;
   __shared__ uint32_t wcnt[2][kSelWaves];
@@ -262,14 +269,94 @@ select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float
       pos += static_cast<uint32_t>(__popcll(bsel & lt_mask));
       if (valid) {
         mask[i] = sel ? 1 : 0;
-        if (sel) idx[pos] = i;
+        if (sel) idx[pos] = idx_base + i;
       }
       base_eq += eq_total;
       base_sel += sel_total;
       __syncthreads();  // wcnt is rewritten by the next chunk
     }
   }
-  if (tid == 0) *n_sel = static_cast<int32_t>(base_sel);
+  if (tid == 0 && n_sel != nullptr) *n_sel = static_cast<int32_t>(base_sel);
+}
+
+template <int R>
+__global__ void __launch_bounds__(kSelThreads)
+select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float threshold,
+            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
+  topk_rows<R>(s, L, k, threshold_mode, threshold, 0, idx, mask, n_sel);
+}
+
+// Two-stage selection: workgroup t handles segment t (tokens [tN, tN + N)).
+// A segment outside the anchor set clears its mask; an anchor segment takes
+// its min(k, N) tokens ranked first by (s desc, index asc) and writes them at
+// idx[a * min(k, N)...], a = the number of anchor segments before it, so idx
+// stays ascending.  Workgroup 0 writes the total count.
+template <int R>
+__global__ void __launch_bounds__(kSelThreads)
+select_segments(const float* __restrict__ s, const uint8_t* __restrict__ anchors, int T, int N, int k,
+                int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
+  __shared__ int sh_before, sh_total;
+  const int t = blockIdx.x, tid = threadIdx.x;
+  if (tid == 0) {
+    sh_before = 0;
+    sh_total = 0;
+  }
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int u = tid; u < T; u += kSelThreads) {
+    const int a = anchors[u] != 0;
+    total += a;
+    before += (u < t) ? a : 0;
+  }
+  if (total) atomicAdd(&sh_total, total);
+  if (before) atomicAdd(&sh_before, before);
+  __syncthreads();
+  const int kk = k < N ? k : N;
+  if (t == 0 && tid == 0) *n_sel = sh_total * kk;
+  const int64_t base = static_cast<int64_t>(t) * N;
+  if (!anchors[t]) {
+    for (int i = tid; i < N; i += kSelThreads) mask[base + i] = 0;
+    return;
+  }
+  topk_rows<R>(s + base, N, kk, 0, 0.0f, static_cast<int>(base), idx + static_cast<int64_t>(sh_before) * kk,
+               mask + base, nullptr);
+}
+
+// Anchor segments, one workgroup, T <= kMaxAnchorT:
+//   mode 0: the k segments ranked first by (key desc, index asc), NaN first
+//           (each segment counts the segments that rank before it);
+//   mode 1: the evenly spaced segments floor((2j + 1) T / (2k)), j < k
+//           (segment t is one iff some j satisfies 2kt <= (2j + 1) T < 2k(t + 1)).
+constexpr int kMaxAnchorT = 4096;
+
+__global__ void __launch_bounds__(kSelThreads)
+anchor_select(const float* __restrict__ keys, int T, int k, int mode, uint8_t* __restrict__ anchors) {
+  __shared__ uint32_t kl[kMaxAnchorT];
+  const int tid = threadIdx.x;
+  if (mode == 0) {
+    for (int t = tid; t < T; t += kSelThreads) kl[t] = rank_key(keys[t]);
+    __syncthreads();
+    for (int t = tid; t < T; t += kSelThreads) {
+      const uint32_t kt = kl[t];
+      int rank = 0;
+      for (int u = 0; u < T; ++u) {
+        const uint32_t ku = kl[u];
+        rank += (ku > kt || (ku == kt && u < t)) ? 1 : 0;
+      }
+      anchors[t] = rank < k ? 1 : 0;
+    }
+    return;
+  }
+  for (int t = tid; t < T; t += kSelThreads) {
+    uint8_t a = 0;
+    if (k > 0) {
+      // smallest j with (2j + 1) T >= 2kt
+      const int64_t num = 2 * static_cast<int64_t>(k) * t - T;
+      const int64_t j = num <= 0 ? 0 : (num + 2 * static_cast<int64_t>(T) - 1) / (2 * static_cast<int64_t>(T));
+      a = (j < k && (2 * j + 1) * T < 2 * static_cast<int64_t>(k) * (t + 1)) ? 1 : 0;
+    }
+    anchors[t] = a;
+  }
 }
 
 hipError_t launch_saliency(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
@@ -319,6 +406,27 @@ hipError_t launch_topk(const float* s, int L, int k, int threshold_mode, float t
 #undef ECHO_SEL_CASE
   return ECHO_LAUNCH("select_rows", select_rows<0>, dim3(1), dim3(kSelThreads), 0, stream, s, L, k,
                      threshold_mode, threshold, idx, mask, n_sel);
+}
+
+hipError_t launch_topk_segments(const float* s, const uint8_t* anchors, int T, int N, int k, int32_t* idx,
+                                uint8_t* mask, int32_t* n_sel, hipStream_t stream) {
+#define ECHO_SEG_CASE(RK)                                                                             \
+  if (N <= RK * kSelThreads)                                                                          \
+    return ECHO_LAUNCH("select_segments", select_segments<RK>, dim3(T), dim3(kSelThreads), 0, stream, s, \
+                       anchors, T, N, k, idx, mask, n_sel);
+  ECHO_SEG_CASE(2)
+  ECHO_SEG_CASE(8)
+  ECHO_SEG_CASE(32)
+#undef ECHO_SEG_CASE
+  return ECHO_LAUNCH("select_segments", select_segments<0>, dim3(T), dim3(kSelThreads), 0, stream, s, anchors,
+                     T, N, k, idx, mask, n_sel);
+}
+
+int max_anchor_segments() { return kMaxAnchorT; }
+
+hipError_t launch_anchors(const float* keys, int T, int k, int mode, uint8_t* anchors, hipStream_t stream) {
+  return ECHO_LAUNCH("anchor_select", anchor_select, dim3(1), dim3(kSelThreads), 0, stream, keys, T, k, mode,
+                     anchors);
 }
 
 hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,

@@ -126,3 +126,37 @@ def test_refcache_rejects_before_launch(lib):
     assert run(ok, state=bad) == _lib.ECHO_EINVAL
     assert lib.echo_refcache_init(ctypes.byref(_lib.RefCacheCfg(40, 64, 0, 8, 44, 0.5)),
                                   ctypes.byref(st), None) == _lib.ECHO_EINVAL
+
+
+def test_anchors_and_segments_reject_before_launch(lib):
+    def anc(keys=FAKE, T=21, k=7, mode=_lib.ECHO_ANCHOR_TOPK, out=FAKE):
+        return lib.echo_anchors(keys, T, k, mode, out, None)
+    assert anc(T=0, k=0) == _lib.ECHO_EINVAL
+    assert anc(T=4097, k=1) == _lib.ECHO_EINVAL
+    assert anc(k=22) == _lib.ECHO_EINVAL
+    assert anc(k=-1) == _lib.ECHO_EINVAL
+    assert anc(mode=2) == _lib.ECHO_EINVAL
+    assert anc(keys=None) == _lib.ECHO_EINVAL                   # top-k needs keys
+    assert anc(keys=MISALIGNED) == _lib.ECHO_EINVAL
+    assert anc(out=None, mode=_lib.ECHO_ANCHOR_UNIFORM) == _lib.ECHO_EINVAL
+
+    def seg(s=FAKE, T=21, N=1560, k=10, idx=FAKE, n=FAKE):
+        return lib.echo_topk_segments(s, FAKE, T, N, k, idx, FAKE, n, None)
+    assert seg(T=0) == _lib.ECHO_EINVAL
+    assert seg(N=0) == _lib.ECHO_EINVAL
+    assert seg(k=-1) == _lib.ECHO_EINVAL
+    assert seg(T=65535, N=40000) == _lib.ECHO_EINVAL            # T * N >= 2^31
+    assert seg(s=MISALIGNED) == _lib.ECHO_EINVAL
+    assert seg(n=None) == _lib.ECHO_EINVAL
+
+
+def test_cache_codec_rejects_before_launch(lib):
+    def run(codec, store=FAKE, codes=FAKE, scale=FAKE, cfg=_lib.CacheCfg(32, 64, 1), n=4):
+        return lib.echo_cache_update_codec(ctypes.byref(cfg), codec, FAKE, FAKE, FAKE, n, FAKE, FAKE,
+                                           store, codes, scale, FAKE, None)
+    assert run(3) == _lib.ECHO_EINVAL
+    assert run(_lib.ECHO_CODEC_FULL, store=None) == _lib.ECHO_EINVAL
+    assert run(_lib.ECHO_CODEC_NAIVE_INT8, codes=None) == _lib.ECHO_EINVAL
+    assert run(_lib.ECHO_CODEC_RESIDUAL_INT8, scale=MISALIGNED) == _lib.ECHO_EINVAL
+    assert run(_lib.ECHO_CODEC_FULL, cfg=_lib.CacheCfg(32, 60, 1)) == _lib.ECHO_EINVAL
+    assert run(_lib.ECHO_CODEC_FULL, n=33) == _lib.ECHO_EINVAL
