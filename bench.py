@@ -12,7 +12,11 @@ tokens), 5.06 s of 16 kHz audio.
 Prints one JSON line: whole-step tokens/s (L / step time), the roofline of the
 dominant kernel measured with HIP events on the launch stream during the timed
 steps, a per-kernel table, and the CPU oracle's throughput on a bounded sample
-(rank 0, N = 1).
+(rank 0, N = 1).  Side legs, outside the timed step: the adaptive reference
+cache (update time, live references and bytes), a scheduled multi-block stack
+over a denoising trajectory, and the module ablation's variants (anchor
+strategies, step-only / latent-only schedules, 16-bit and naive int8 caches:
+kernel times, stack latency, cache bytes, distance from an all-full run).
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 """
@@ -32,7 +36,8 @@ if ROOT not in sys.path:
 METRIC = "latent tokens/s per cached DiT block step + %MFMA / %HBM peak"
 KERNEL_SOURCES = {"attn_fwd": "attn_bf16.hip", "gemm_": "gemm_bf16.hip", "saliency": "select.hip",
                   "select": "select.hip", "cache_update": "cache.hip", "modln": "block_ln.hip",
-                  "energy": "energy.hip", "refcache": "refcache.hip"}
+                  "energy": "energy.hip", "refcache": "refcache.hip",
+                  "anchor": "select.hip"}
 
 
 def log(msg: str) -> None:
@@ -189,19 +194,13 @@ def refcache_leg(w, dev, dt, steps: int = 5, tau: float = 0.9, corr: float = 0.9
                     "latent-grid row"}
 
 
-def stack_leg(w, dev, dt, fw, n_blocks: int, steps: int, n_full: int = 2, r_min: float = 0.2,
-              r_max: float = 0.6, alpha: float = 0.4):
-    """A stack of n_blocks blocks of the workload's shape over a synthetic
-    denoising trajectory of first-block inputs x_{t+1} = x_t + (0.3 / (t + 1)) N(0, 1):
-    one Eq. 1 value and one selection per step on the first block's input, K from
-    the step schedule, then every block on the shared selection.  Random-init
-    weights (generated on the device, same distributions as the main step)."""
+def make_stack_blocks(w, dev, dt, n_blocks: int, seed: int):
+    """Random-init weights of n_blocks blocks of the workload's shape,
+    generated on the device (same distributions as the main step)."""
     import torch
 
-    from paper_2608_02474_amd import api
-
     g = torch.Generator(device=dev)
-    g.manual_seed(2000 + w.seed)
+    g.manual_seed(seed)
     D, F = w.D, w.F
 
     def rnd(*shape, std=0.02, mean=0.0, dtype=dt):
@@ -214,23 +213,55 @@ def stack_leg(w, dev, dt, fw, n_blocks: int, steps: int, n_full: int = 2, r_min:
         blocks.append({"wq": rnd(D, D), "wk": rnd(D, D), "wv": rnd(D, D), "wo": rnd(D, D),
                        "w1": rnd(F, D), "w2": rnd(D, F), "bq": rnd(D), "bk": rnd(D), "bv": rnd(D),
                        "bo": rnd(D), "b1": rnd(F), "b2": rnd(D), "mod": mod.contiguous()})
-    stack = api.BlockStack(blocks, w.H, w.L, D, dev, dt, api.Scheduler(n_full, r_min, r_max, alpha))
-    x = torch.randn((w.L, D), device=dev, generator=g)
-    times = []
+    return blocks
+
+
+def run_trajectory(stack, w, dev, dt, fw, steps: int, seed: int, motion=None, ref=None, keep=False):
+    """First-block inputs x_{t+1} = x_t + (0.3 / (t + 1)) m N(0, 1), generated on
+    the device from `seed`, m = motion[frame of the token] (1 if None).
+    Returns (per-step ms, outputs): every step's output if keep, else the
+    relative L2 distance of every step's output from ref[t] if ref is given,
+    else the last output."""
+    import torch
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    x = torch.randn((w.L, w.D), device=dev, generator=g)
+    m = None if motion is None else motion.repeat_interleave(w.N)[:, None]
+    times, outs, y = [], [], None
     for t in range(steps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        stack.step(x.to(dt), fw, w.N)
+        y = stack.step(x.to(dt), fw, w.N)
         e1.record()
         torch.cuda.synchronize()
         times.append(e0.elapsed_time(e1))
-        x = x + torch.randn((w.L, D), device=dev, generator=g) * (0.3 / (t + 1))
+        if keep:
+            outs.append(y.clone())
+        elif ref is not None:
+            r = ref[t].float()
+            outs.append(float(torch.linalg.vector_norm(y.float() - r) / torch.linalg.vector_norm(r)))
+        dx = torch.randn((w.L, w.D), device=dev, generator=g) * (0.3 / (t + 1))
+        x = x + (dx if m is None else dx * m)
+    return times, (outs if keep or ref is not None else y)
+
+
+def stack_leg(w, dev, dt, fw, blocks, steps: int, n_full: int = 2, r_min: float = 0.2,
+              r_max: float = 0.6, alpha: float = 0.4):
+    """A stack of blocks of the workload's shape over a synthetic denoising
+    trajectory: one Eq. 1 value and one selection per step on the first
+    block's input, K from the step schedule, then every block on the shared
+    selection."""
+    from paper_2608_02474_amd import api
+
+    stack = api.BlockStack(blocks, w.H, w.L, w.D, dev, dt, api.Scheduler(n_full, r_min, r_max, alpha))
+    times, _ = run_trajectory(stack, w, dev, dt, fw, steps, seed=3000 + w.seed)
     ks = [k for k, _, _ in stack.history]
     full = [f for _, f, _ in stack.history]
     full_ms = [tm for tm, f in zip(times, full) if f]
     cached_ms = [tm for tm, f in zip(times, full) if not f]
     ref = sum(full_ms) / len(full_ms)
-    return {"blocks": n_blocks, "steps": steps,
+    return {"blocks": len(blocks), "steps": steps,
             "schedule": {"n_full": n_full, "r_min": r_min, "r_max": r_max, "alpha": alpha},
             "k_per_step": ks, "full_step": full,
             "delta_per_step": [None if f else round(d, 6) for _, f, d in stack.history],
@@ -242,6 +273,150 @@ def stack_leg(w, dev, dt, fw, n_blocks: int, steps: int, n_full: int = 2, r_min:
             "data": "synthetic trajectory and random-init weights (device-generated)"}
 
 
+def _kernel_avgs(ktimes: dict) -> dict:
+    return {n: t / c for n, (c, t) in ktimes.items()}
+
+
+def variants_leg(w, dev, dt, fe, fw, blocks, steps: int, n_anchor: int = 14, n_full: int = 2,
+                 r_min: float = 0.2, r_max: float = 0.6, alpha: float = 0.4, refresh: float = 0.4):
+    """The module ablation's variants (anchor strategies, schedules, cache
+    codecs) on the workload's shape: their kernels alone, then stacks of the
+    same blocks over the same trajectory, each with its latency, cache bytes
+    and the relative L2 distance of its last output from an all-full run."""
+    import torch
+
+    from paper_2608_02474_amd import api, roofline
+
+    L, D, N, T, K = w.L, w.D, w.N, w.T, w.K
+    b = 2 if dt == torch.bfloat16 else 4
+    g = torch.Generator(device=dev)
+    g.manual_seed(4000 + w.seed)
+    out = {}
+
+    # (1) the cache codecs alone: one full write, then updates at K rows
+    X = torch.randn((L, D), device=dev, generator=g).to(dt)
+    perm = torch.randperm(L, device=dev, generator=g)[:K]
+    idx = torch.sort(perm).values.to(torch.int32)
+    mask = torch.zeros(L, dtype=torch.uint8, device=dev)
+    mask[idx.long()] = 1
+    all_idx = torch.arange(L, dtype=torch.int32, device=dev)
+    all_mask = torch.ones(L, dtype=torch.uint8, device=dev)
+    y_all = torch.randn((L, D), device=dev, generator=g)
+    y_sel = y_all[:K].contiguous()
+    work = roofline.kernel_work(L, K, D, w.F, b)
+    codecs = {}
+    for cname, codec in (("residual_int8", 0), ("full", 1), ("naive_int8", 2)):
+        st = dict(store=torch.zeros((L, D), dtype=dt, device=dev)) if codec == 1 else dict(
+            codes=torch.zeros((L, D), dtype=torch.int8, device=dev), scale=torch.zeros(L, device=dev))
+        xref = torch.zeros((L, D), dtype=dt, device=dev)
+        y = torch.empty((L, D), dtype=dt, device=dev)
+        api.cache_update_codec(codec, X, all_idx, all_mask, L, y_all, xref, y, **st)
+        for _ in range(3):
+            api.cache_update_codec(codec, X, idx, mask, K, y_sel, xref, y, **st)
+        torch.cuda.synchronize()
+        api.profile_enable(True)
+        api.profile_read()
+        for _ in range(20):
+            api.cache_update_codec(codec, X, idx, mask, K, y_sel, xref, y, **st)
+        avgs = _kernel_avgs(api.profile_read())
+        api.profile_enable(False)
+        kname, avg = next(iter(avgs.items()))
+        amount, _ = roofline.work_of(kname, work)
+        gbs = amount / (avg * 1e-3) / 1e9
+        state = L * D * b + sum(t.numel() * t.element_size() for t in st.values())
+        codecs[cname] = {"kernel": kname, "avg_ms": round(avg, 4), "achieved_gbs": round(gbs, 1),
+                         "frac": round(gbs / roofline.PEAK_HBM_GBS, 4), "per_launch": amount,
+                         "cache_bytes_per_block": state}
+        del st, xref, y
+    out["codec_kernels"] = codecs
+    del X, y_all, y_sel
+
+    # (2) selection: anchors once per clip; two-stage vs global top-k per step
+    keys = torch.rand(T, device=dev, generator=g)
+    sal = torch.rand(L, device=dev, generator=g)
+    sel = api.Selection(idx=torch.empty(L, dtype=torch.int32, device=dev),
+                        mask=torch.empty(L, dtype=torch.uint8, device=dev),
+                        n_sel_dev=torch.empty(1, dtype=torch.int32, device=dev), n_sel=None,
+                        saliency=sal, step_delta=None)
+    kseg = api.topk_count(w.ratio, N)
+    am = api.anchors(T, n_anchor, "random", keys=keys)
+    for _ in range(3):
+        api.topk_segments(sel, am, N, kseg)
+        api.topk(sel, N, D, dt, k=n_anchor * kseg)
+    torch.cuda.synchronize()
+    api.profile_enable(True)
+    api.profile_read()
+    for _ in range(20):
+        api.anchors(T, n_anchor, "random", keys=keys, out=am)
+        api.topk_segments(sel, am, N, kseg)
+        api.topk(sel, N, D, dt, k=n_anchor * kseg)
+    avgs = _kernel_avgs(api.profile_read())
+    api.profile_enable(False)
+    out["selection_kernels"] = {"anchors": n_anchor, "tokens_per_anchor": kseg,
+                                "selected": n_anchor * kseg,
+                                "anchor_select_ms": round(avgs.get("anchor_select", 0.0), 4),
+                                "select_segments_ms": round(avgs.get("select_segments", 0.0), 4),
+                                "select_rows_ms_same_count": round(avgs.get("select_rows", 0.0), 4)}
+
+    # (3) stacks: the same blocks and trajectory under each variant.  The
+    # trajectory's per-frame change follows the audio energy (m_t = 0.2 + 0.8
+    # w_t, w = frame weight): the premise of the energy anchors.
+    unit = torch.ones(T, device=dev)
+    motion = 0.2 + 0.8 * fw
+    anchor_masks = {"energy": api.anchors(T, n_anchor, "energy", keys=fe),
+                    "uniform": api.anchors(T, n_anchor, "uniform", device=dev),
+                    "random": api.anchors(T, n_anchor, "random",
+                                          keys=torch.rand(T, device=dev, generator=g))}
+    sched = lambda: api.Scheduler(n_full, r_min, r_max, alpha)
+    configs = [
+        ("all_full", dict(scheduler=api.Scheduler(steps, 1.0, 1.0, 0.0))),
+        ("echocache", dict(scheduler=sched())),
+        ("unit_frame_weight", dict(scheduler=sched(), fw=unit)),
+        ("two_stage_energy", dict(scheduler=sched(), anchor_mask=anchor_masks["energy"])),
+        ("two_stage_uniform", dict(scheduler=sched(), anchor_mask=anchor_masks["uniform"])),
+        ("two_stage_random", dict(scheduler=sched(), anchor_mask=anchor_masks["random"])),
+        ("step_only", dict(scheduler=api.Scheduler.step_only(n_full, refresh))),
+        ("latent_only", dict(scheduler=api.Scheduler.latent_only(n_full, w.ratio))),
+        ("fp16_cache", dict(scheduler=sched(), codec="full")),
+        ("naive_int8_cache", dict(scheduler=sched(), codec="naive_int8")),
+    ]
+    runs, ref = {}, None
+    for name, cfg in configs:
+        log(f"  variant stack {name}")
+        f = cfg.pop("fw", fw)
+        stack = api.BlockStack(blocks, w.H, L, D, dev, dt, cfg.pop("scheduler"), **cfg)
+        if ref is None:
+            times, ref = run_trajectory(stack, w, dev, dt, f, steps, 5000 + w.seed, motion, keep=True)
+            errs = [0.0] * steps
+        else:
+            times, errs = run_trajectory(stack, w, dev, dt, f, steps, 5000 + w.seed, motion, ref=ref)
+        two = cfg.get("anchor_mask") is not None
+        cached = [e for e, (_, full, _) in zip(errs, stack.history) if not full]
+        runs[name] = {"trajectory_ms": round(sum(times), 1),
+                      "tokens_recomputed": int(sum(L if full else (n_anchor * min(k, N) if two else k)
+                                                   for k, full, _ in stack.history)),
+                      "full_steps": int(sum(full for _, full, _ in stack.history)),
+                      "cache_bytes_per_block": stack.cache_bytes() // len(blocks),
+                      "rel_l2_vs_all_full_mean": round(sum(errs) / steps, 5),
+                      "rel_l2_vs_all_full_cached_steps_mean": round(sum(cached) / max(len(cached), 1), 5),
+                      "rel_l2_vs_all_full_max": round(max(errs), 5)}
+        del stack
+        torch.cuda.empty_cache()
+    ref = None
+    base = runs["all_full"]["trajectory_ms"]
+    for r in runs.values():
+        r["speedup_vs_all_full"] = round(base / r["trajectory_ms"], 3)
+    out["stacks"] = {"blocks": len(blocks), "steps": steps, "anchors": n_anchor,
+                     "schedule": {"n_full": n_full, "r_min": r_min, "r_max": r_max, "alpha": alpha,
+                                  "step_only_refresh": refresh, "latent_only_ratio": w.ratio},
+                     "runs": runs,
+                     "data": "synthetic trajectory whose per-frame change scales with the audio "
+                             "energy (0.2 + 0.8 w_t) and random-init weights (device-generated); the "
+                             "distance from the all-full outputs is a numerical proxy, not the "
+                             "paper's video-quality metrics"}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -251,6 +426,9 @@ def main() -> int:
     ap.add_argument("--stack-blocks", type=int, default=40,
                     help="blocks of the stack leg (the scheduled multi-block trajectory); 0: skip")
     ap.add_argument("--stack-steps", type=int, default=10)
+    ap.add_argument("--variant-blocks", type=int, default=10,
+                    help="blocks of the ablation-variants leg (anchors, schedules, codecs); 0: skip")
+    ap.add_argument("--variant-steps", type=int, default=10)
     ap.add_argument("--skip-cpu-baseline", action="store_true",
                     help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
                          "unchanged")
@@ -366,12 +544,19 @@ def main() -> int:
 
     log("adaptive reference cache leg")
     out["refcache"] = refcache_leg(w, dev, dt)
-    if args.stack_blocks > 0:
-        log(f"stack leg: {args.stack_blocks} blocks, {args.stack_steps} steps")
+    if args.stack_blocks > 0 or args.variant_blocks > 0:
         blk = None                             # free the main step's block and workspace
         torch.cuda.empty_cache()
-        _, _, fw_stack = api.energy(A, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
-        out["stack"] = stack_leg(w, dev, dt, fw_stack, args.stack_blocks, args.stack_steps)
+        _, fe_stack, fw_stack = api.energy(A, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
+        blocks = make_stack_blocks(w, dev, dt, max(args.stack_blocks, args.variant_blocks), 2000 + w.seed)
+        if args.stack_blocks > 0:
+            log(f"stack leg: {args.stack_blocks} blocks, {args.stack_steps} steps")
+            out["stack"] = stack_leg(w, dev, dt, fw_stack, blocks[:args.stack_blocks], args.stack_steps)
+        if args.variant_blocks > 0:
+            log(f"variants leg: {args.variant_blocks} blocks, {args.variant_steps} steps")
+            out["variants"] = variants_leg(w, dev, dt, fe_stack, fw_stack, blocks[:args.variant_blocks],
+                                           args.variant_steps)
+        blocks = None
 
     if args.skip_cpu_baseline:
         out["cpu_baseline"] = None

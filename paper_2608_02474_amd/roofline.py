@@ -25,6 +25,7 @@ def kernel_work(L: int, K: int, D: int, F: int, b: int, n_samples: int = 0):
         "saliency_rows": (2 * L * D * b + 20 * L, "byte"),
         # selection: a few passes over 4-byte keys (latency-bound); write idx, mask
         "select_rows": (4 * L + 4 * K + L, "byte"),
+        "select_segments": (4 * L + 4 * K + L, "byte"),
         # LN1 over all rows: read x, write a
         "modln_in": (2 * L * D * b, "byte"),
         "gemm_q": (2 * K * D * D, "flop"),
@@ -35,6 +36,11 @@ def kernel_work(L: int, K: int, D: int, F: int, b: int, n_samples: int = 0):
         "modln_x1": (K * D * (4 + b), "byte"),
         "gemm_ffn_up": (2 * K * D * F, "flop"),
         "gemm_ffn_down": (2 * K * F * D, "flop"),
+        # 16-bit output cache: fresh rows read y_sel and x, write y, xref and the
+        # stored row; reused rows copy their stored row to y; plus the mask
+        "cache_update_full": (K * D * (4 + 4 * b) + U * D * 2 * b + L, "byte"),
+        # naive int8: as the residual cache, but reused rows read no reference
+        "cache_update_naive": (K * D * (4 + b + b + 1 + b) + U * D * (1 + b) + 4 * L + L, "byte"),
         # cache update: fresh rows read y_sel (fp32) and x, write xref, codes, y;
         # reused rows read xref and codes and write y; plus scale and mask
         "cache_update": (K * D * (4 + b + b + 1 + b) + U * D * (b + 1 + b) + 4 * L + L, "byte"),
