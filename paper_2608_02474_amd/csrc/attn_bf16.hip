@@ -7,7 +7,7 @@
 // one head (each wave QB blocks of 32 queries).  Keys stream in tiles of 64:
 //   * K and V tiles are copied HBM/L2 -> LDS by direct global-to-LDS loads
 //     (global_load_lds_dwordx4: no VGPR staging), row-major [key][dh], into a
-//     3-stage ring.  Each lane fetches the 16-byte piece whose swizzled LDS
+//     4-stage ring.  Each lane fetches the 16-byte piece whose swizzled LDS
 //     slot is its own lane slot, so the XOR swizzles cost nothing at load time.
 //   * S^T (keys x queries) = K_tile . Q^T with v_mfma_f32_32x32x16_bf16; the
 //     query fragments stay in registers for the whole key loop; K rows enter
@@ -25,6 +25,10 @@
 //   * O^T (dh x queries) += V^T . P^T: P^T is the S accumulator converted to
 //     bf16 in registers; V^T fragments come straight from the row-major V tile
 //     with ds_read_b64_tr_b16 (LDS transpose reads), two per 8-key operand.
+//   * The key loop is software-pipelined by one tile: the exp / pack / row
+//     sum of tile t is spread between the MFMAs of S(t+1), and the row maximum
+//     of S(t+1) between the MFMAs of PV(t), so each wave's vector work runs
+//     under its own matrix work (two accumulator sets for S).
 // Workgroup ids are remapped so that each XCD works through a contiguous range
 // of (head, query-tile) pairs: the query tiles of one head share that head's
 // K/V stream in one L2.
@@ -40,7 +44,10 @@ namespace echo {
 
 constexpr int ATT_KT = 64, ATT_DH = 128;
 constexpr int ATT_TILE_BYTES = ATT_KT * ATT_DH * 2;  // one K or V tile: 16 KB
-constexpr int ATT_STAGE_BYTES = 2 * ATT_TILE_BYTES;  // K + V
+constexpr int ATT_NSTAGE = 4;                         // K/V ring stages
+// LDS: the K tiles of the 4 stages, then the V tiles of the 4 stages, so
+// that every fragment read is a base register plus a 16-bit immediate offset
+constexpr int ATT_V_BASE = ATT_NSTAGE * ATT_TILE_BYTES;  // 64 KB
 constexpr int ATT_OS_STRIDE = ATT_DH + 8;            // output staging row (bf16)
 constexpr float ATT_RESCALE_LOG2 = 8.0f;             // lazy-rescale headroom (log2 units)
 constexpr int ATT_RING = 2;                          // LDS fragment reads in flight per wave
@@ -48,15 +55,13 @@ constexpr int ATT_RING = 2;                          // LDS fragment reads in fl
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// Per tile: barrier -> S -> softmax -> PV; the two waves of a SIMD overlap
-// each other's LDS latency and vector work.
+// Four K/V stages: tile t + 3 is copied while S(t+1) and PV(t) run.
 template <int QB, int WAVES>
 struct AttCfg {
   static constexpr int kThreads = WAVES * 64;
   static constexpr int kQ = WAVES * QB * 32;  // queries per workgroup
-  static constexpr int kStages = 3;
-  static constexpr int kLdsBytes = (kStages * ATT_STAGE_BYTES > kQ * ATT_OS_STRIDE * 2)
-                                       ? kStages * ATT_STAGE_BYTES
+  static constexpr int kLdsBytes = (2 * ATT_V_BASE > kQ * ATT_OS_STRIDE * 2)
+                                       ? 2 * ATT_V_BASE
                                        : kQ * ATT_OS_STRIDE * 2;
 };
 
@@ -71,6 +76,15 @@ __device__ __forceinline__ int k_slot(int r, int c) { return c ^ perm23(r & 15);
 // serves) touches 4 consecutive rows of the logical blocks 2d and 2d+1; these
 // 8 pieces land in the 8 distinct physical blocks.
 __device__ __forceinline__ int v_block(int r, int b) { return b ^ ((r & 3) << 1); }
+
+// one of two register sets, chosen at compile time
+template <int I, typename T>
+__device__ __forceinline__ T& pick2(T& a, T& b) {
+  if constexpr (I == 0)
+    return a;
+  else
+    return b;
+}
 
 __device__ __forceinline__ float pair_max(float x) {
   // max over lanes l and l^32
@@ -93,7 +107,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
               bf16_t* __restrict__ out, int64_t ldo, int item_base, int nsplit, int kt_per_split,
               float* __restrict__ part_o, float* __restrict__ part_ml) {
   typedef AttCfg<QB, WAVES> C;
-  constexpr int ATT_NSTAGE = C::kStages;
   constexpr int NLD = 16 / WAVES;  // 1 KB direct-load instructions per wave per K (or V) tile
   static_assert(16 % WAVES == 0, "16 KB tiles split evenly over the waves");
   __shared__ __attribute__((aligned(1024))) char smem[C::kLdsBytes];
@@ -134,49 +147,51 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
 #pragma unroll
     for (int s = 0; s < 8; ++s) qf[b][s] = __builtin_bit_cast(bf16x8, ldg16(src + 16 * s));
   }
+  // The query loads are the only memory reads the compiler tracks (the tile
+  // copies are inline assembly): waiting for them here keeps it from placing
+  // vmcnt waits before their first use inside the loop, where the hardware
+  // counter also holds the copies of the next two tiles.
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
   // ---- direct-load plan: instruction n of this wave fills tile rows 4m .. 4m+3
   // (m = wave + WAVES n); the lane lands in row 4m + lane/16, slot lane%16.
-  int k_src[NLD], v_src[NLD], ld_row[NLD], k_off[NLD], v_off[NLD];
+  uint32_t row_off[NLD];             // byte offset of the lane's row within a tile
+  uint32_t k_src[NLD], v_src[NLD];   // byte offsets within a row
 #pragma unroll
   for (int n = 0; n < NLD; ++n) {
     const int r = 4 * (wave + WAVES * n) + g16;
     const int p = i16;
     const int ck = k_slot(r, p);                      // the XOR is its own inverse
     const int cv = 2 * v_block(r, p >> 1) + (p & 1);
-    ld_row[n] = r;
-    k_src[n] = ck * 8;
-    v_src[n] = cv * 8;
-    k_off[n] = r * static_cast<int>(ldkv) + ck * 8;   // element offsets within a tile
-    v_off[n] = r * static_cast<int>(ldkv) + cv * 8;
+    row_off[n] = static_cast<uint32_t>(r) * static_cast<uint32_t>(ldkv) * 2u;
+    k_src[n] = static_cast<uint32_t>(ck * 16);
+    v_src[n] = static_cast<uint32_t>(cv * 16);
   }
   const bf16_t* kh = k + hoff;
   const bf16_t* vh = v + hoff;
   const uint32_t lds0 = lds_offset(smem);
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  // Copies of relative tile t into a stage.  Branch-free: the tile start is
+  // part of the uniform base and each lane clamps its row offset to the row
+  // L - 1 (rows past L are finite copies of row L - 1, masked later); a tile
+  // index past the last tile re-copies the last tile (into a stage that is
+  // free), so every wave always has the copies of exactly two tiles in flight
+  // after an issue and one wait count fits every iteration.
+  const uint32_t ldkv2 = static_cast<uint32_t>(ldkv) * 2u;
   auto issue_tile = [&](int t, int stage) __attribute__((always_inline)) {
-    const int key0 = t * ATT_KT;
-    const uint32_t kdst = lds0 + stage * ATT_STAGE_BYTES;
-    const uint32_t vdst = kdst + ATT_TILE_BYTES;
-    if (key0 + ATT_KT <= L) {  // full tile: uniform tile base + per-lane offsets
-      const bf16_t* kt = kh + static_cast<int64_t>(key0) * ldkv;
-      const bf16_t* vt = vh + static_cast<int64_t>(key0) * ldkv;
-#pragma unroll
-      for (int n = 0; n < NLD; ++n) {
-        const uint32_t m = static_cast<uint32_t>(wave_u + WAVES * n);
-        lds_copy16(kt + k_off[n], kdst + m * 1024);
-        lds_copy16(vt + v_off[n], vdst + m * 1024);
-      }
-      return;
-    }
+    t = t < nkt ? t : nkt - 1;
+    const int key0 = (t_begin + t) * ATT_KT;
+    const bf16_t* kt = kh + static_cast<int64_t>(key0) * ldkv;
+    const bf16_t* vt = vh + static_cast<int64_t>(key0) * ldkv;
+    const uint32_t last = static_cast<uint32_t>(L - 1 - key0) * ldkv2;  // offset of row L - 1
+    const uint32_t kdst = lds0 + stage * ATT_TILE_BYTES;
+    const uint32_t vdst = kdst + ATT_V_BASE;
 #pragma unroll
     for (int n = 0; n < NLD; ++n) {
       const uint32_t m = static_cast<uint32_t>(wave_u + WAVES * n);
-      int row = key0 + ld_row[n];
-      row = row < L ? row : L - 1;  // ragged last tile: re-read row L-1 (finite, masked later)
-      const int64_t rofs = static_cast<int64_t>(row) * ldkv;
-      lds_copy16(kh + rofs + k_src[n], kdst + m * 1024);
-      lds_copy16(vh + rofs + v_src[n], vdst + m * 1024);
+      const uint32_t ro = row_off[n] < last ? row_off[n] : last;
+      lds_copy16_s(kt, ro + k_src[n], kdst + m * 1024);
+      lds_copy16_s(vt, ro + v_src[n], vdst + m * 1024);
     }
   };
 
@@ -198,7 +213,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     for (int t = 0; t < 2; ++t) {
       const int rlow = 8 * (g16 >> 1) + 4 * t + (i16 >> 2);  // row within the 16-key step
       const int blk = v_block(rlow, 2 * d + (g16 & 1));
-      v_rd[d][t] = ATT_TILE_BYTES + rlow * 256 + blk * 32 + 8 * (i16 & 3);
+      v_rd[d][t] = ATT_V_BASE + rlow * 256 + blk * 32 + 8 * (i16 & 3);
     }
 
   f32x16 o[QB][4];
@@ -216,62 +231,85 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
 
   const f32x16 zero16 = {};
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+
+  // The key loop works in halves of 32 keys: half h is key block kb = h % 2
+  // of tile h / 2.  A lane holds 16 scores of a half per query block (its
+  // accumulator column; lanes l and l ^ 32 share a query).
+  //
+  // K fragment of S step st (k16 block of dh) for key block kb of a stage
+  auto read_k = [&](const char* ks, int kb, int st) __attribute__((always_inline)) {
+    return *reinterpret_cast<const bf16x8*>(ks + kb * 32 * 256 + k_rd[st]);
+  };
+  // V^T fragment of PV step (d, a) for key block kb: dh block d, 16-key half a
+  auto read_v = [&](const char* vs, int kb, int d, int a) __attribute__((always_inline)) {
+    const int step = (kb * 32 + 16 * a) * 256;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][0]));
+    const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][1]));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
   // Fragments flow through a ring of ATT_RING registers: the read for step
   // i + ATT_RING is issued right after the MFMA of step i has taken its
   // operand, so every MFMA finds its fragment ATT_RING steps old.
-  auto compute_s = [&](auto stage_c, f32x16(&sacc)[2][QB]) __attribute__((always_inline)) {
-    constexpr int STAGE = decltype(stage_c)::value;
-    const char* ks = smem + STAGE * ATT_STAGE_BYTES;
+  //
+  // S of one half (8 MFMAs) with `work(i)` placed after MFMA i
+  auto s_half = [&](const char* ks, int kb, f32x16(&sh)[QB], auto&& work) __attribute__((always_inline)) {
     bf16x8 ring[ATT_RING];
 #pragma unroll
-    for (int i = 0; i < ATT_RING; ++i)
-      ring[i] = *reinterpret_cast<const bf16x8*>(ks + (i / 8) * 32 * 256 + k_rd[i % 8]);
+    for (int i = 0; i < ATT_RING; ++i) ring[i] = read_k(ks, kb, i);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {  // step i: key block kb = i / 8, k16-step s = i % 8
-      const int kb = i / 8, st = i % 8;
+    for (int i = 0; i < 8; ++i) {
       const bf16x8 a = ring[i % ATT_RING];
 #pragma unroll
       for (int b = 0; b < QB; ++b)
-        sacc[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[b][st], st == 0 ? zero16 : sacc[kb][b], 0, 0, 0);
-      const int n = i + ATT_RING;
-      if (n < 16)
-        ring[i % ATT_RING] = *reinterpret_cast<const bf16x8*>(ks + (n / 8) * 32 * 256 + k_rd[n % 8]);
-      __builtin_amdgcn_sched_barrier(0);  // keep the reads ATT_RING steps ahead
+        sh[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[b][i], i == 0 ? zero16 : sh[b], 0, 0, 0);
+      if (i + ATT_RING < 8) ring[i % ATT_RING] = read_k(ks, kb, i + ATT_RING);
+      work(i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // O += V^T P^T for one half (8 MFMAs: dh block d = i / 2, 16-key half
+  // a = i % 2) with `work(i)` placed after MFMA i
+  auto pv_half = [&](const char* vs, int kb, const bf16x8(&pf)[QB][2], auto&& work) __attribute__((always_inline)) {
+    bf16x8 ring[ATT_RING];
+#pragma unroll
+    for (int i = 0; i < ATT_RING; ++i) ring[i] = read_v(vs, kb, i / 2, i % 2);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int d = i / 2, a = i % 2;
+      const bf16x8 va = ring[i % ATT_RING];
+#pragma unroll
+      for (int b = 0; b < QB; ++b)
+        o[b][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[b][a], o[b][d], 0, 0, 0);
+      if (i + ATT_RING < 8) ring[i % ATT_RING] = read_v(vs, kb, (i + ATT_RING) / 2, (i + ATT_RING) % 2);
+      work(i);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // ---- softmax, in four parts so that the pipelined loop can place them apart
-  auto mask_tail = [&](f32x16(&sacc)[2][QB], int key0) __attribute__((always_inline)) {
-    // ragged last tile: keys past L get -inf
+  // keys past L (ragged last tile) get -inf; keyh = first key of the half
+  auto mask_half = [&](f32x16(&sh)[QB], int keyh) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int r = 0; r < 16; ++r) {
+      const bool valid = keyh + 16 * (r >> 3) + 8 * hi + (r & 7) < L;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const bool valid = key0 + kb * 32 + 16 * (r >> 3) + 8 * hi + (r & 7) < L;
-#pragma unroll
-        for (int b = 0; b < QB; ++b) sacc[kb][b][r] = valid ? sacc[kb][b][r] : -INFINITY;
-      }
-  };
-  // tile maximum of each query (lane pair l, l^32 holds one query column)
-  auto tile_max = [&](const f32x16(&sacc)[2][QB], float(&mx)[QB]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < QB; ++b) {
-      float m = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[kb][b][r]);
-      mx[b] = pair_max(m);
+      for (int b = 0; b < QB; ++b) sh[b][r] = valid ? sh[b][r] : -INFINITY;
     }
+  };
+  // running maximum of elements 2c, 2c + 1 (chunk c of 8)
+  auto max_chunk = [&](const f32x16(&sh)[QB], int c, float(&m)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) m[b] = fmaxf(fmaxf(m[b], sh[b][2 * c]), sh[b][2 * c + 1]);
   };
   // lazy rescale: only rows whose maximum grows by more than 2^8 move their
   // reference; the others keep it (alpha = 1, untouched)
-  auto update_max = [&](const float(&mx)[QB]) __attribute__((always_inline)) {
+  auto update_max = [&](const float(&m)[QB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      const bool grow = (mx[b] - m_run[b]) * scale_log2 > ATT_RESCALE_LOG2;
+      const float mx = pair_max(m[b]);
+      const bool grow = (mx - m_run[b]) * scale_log2 > ATT_RESCALE_LOG2;
       if (__builtin_expect(__ballot(grow) != 0ull, 0)) {
-        const float m_new = grow ? mx[b] : m_run[b];
+        const float m_new = grow ? mx : m_run[b];
         const float alpha = grow ? __builtin_amdgcn_exp2f((m_run[b] - m_new) * scale_log2) : 1.0f;
         m_run[b] = m_new;
         l_run[b] *= alpha;
@@ -282,99 +320,128 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       }
     }
   };
-  // probabilities as bf16 MFMA operands; the row sum adds the same bf16
-  // values, two per v_dot2 (fp32 accumulation)
-  auto probs = [&](const f32x16(&sacc)[2][QB], bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
+  // probabilities of elements 8a + j, 8a + j + 1 (chunk c of 8: a = c / 4,
+  // j = 2 (c % 4)): exp2 of the scaled, shifted scores, packed to bf16 (the
+  // PV operand), and the row sum of the same bf16 values, two per v_dot2
+  auto exp_chunk = [&](const f32x16(&sh)[QB], int c, const float(&neg_mc)[QB], float(&psum)[QB],
+                       bf16x8(&pf)[QB][2]) __attribute__((always_inline)) {
+    const int a = c / 4, j = 2 * (c % 4);
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      const float neg_mc = -m_run[b] * scale_log2;
-      const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-      float psum = 0.0f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int a = 0; a < 2; ++a) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            pf[b][kb][a][j] = static_cast<__bf16>(
-                __builtin_amdgcn_exp2f(fmaf(sacc[kb][b][8 * a + j], scale_log2, neg_mc)));
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const bf16x2 pair = {pf[b][kb][a][2 * j], pf[b][kb][a][2 * j + 1]};
-            psum = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, psum, false);
-          }
-        }
-      l_run[b] += psum;
+      pf[b][a][j] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sh[b][8 * a + j], scale_log2, neg_mc[b])));
+      pf[b][a][j + 1] =
+          static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sh[b][8 * a + j + 1], scale_log2, neg_mc[b])));
+      const bf16x2 pair = {pf[b][a][j], pf[b][a][j + 1]};
+      psum[b] = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, psum[b], false);
     }
   };
-  auto softmax = [&](f32x16(&sacc)[2][QB], int key0, bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
-    if (key0 + ATT_KT > L) mask_tail(sacc, key0);
-    float mx[QB];
-    tile_max(sacc, mx);
-    update_max(mx);
-    probs(sacc, pf);
-  };
-
-  auto pv = [&](auto stage_c, const bf16x8(&pf)[QB][2][2]) __attribute__((always_inline)) {
-    constexpr int STAGE = decltype(stage_c)::value;
-    const char* vs = smem + STAGE * ATT_STAGE_BYTES;
-    // step i: dh block d = i / 4, key block kb = (i / 2) % 2, 16-key half a = i % 2
-    auto read_v = [&](int i) __attribute__((always_inline)) {
-      const int d = i / 4, kb = (i / 2) % 2, a = i % 2;
-      const int step = (kb * 32 + 16 * a) * 256;
-      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][0]));
-      const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][1]));
-      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
-    };
-    bf16x8 ring[ATT_RING];
+  auto exp_begin = [&](float(&neg_mc)[QB], float(&psum)[QB]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < ATT_RING; ++i) ring[i] = read_v(i);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int d = i / 4, kb = (i / 2) % 2, a = i % 2;
-      const bf16x8 va = ring[i % ATT_RING];
-#pragma unroll
-      for (int b = 0; b < QB; ++b)
-        o[b][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[b][kb][a], o[b][d], 0, 0, 0);
-      if (i + ATT_RING < 16) ring[i % ATT_RING] = read_v(i + ATT_RING);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int b = 0; b < QB; ++b) {
+      neg_mc[b] = -m_run[b] * scale_log2;
+      psum[b] = 0.0f;
     }
   };
-
-  auto softmax_pv = [&](auto stage_c, f32x16(&sacc)[2][QB], int key0) __attribute__((always_inline)) {
-    bf16x8 pf[QB][2][2];
-    softmax(sacc, key0, pf);
-    pv(stage_c, pf);
+  auto exp_end = [&](const float(&psum)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) l_run[b] += psum[b];
   };
 
-  // tiles are counted from t_begin below: t is relative, t_begin + t absolute
-  issue_tile(t_begin, 0);
-  if (nkt > 1) issue_tile(t_begin + 1, 1);
-
+  // ---- the key loop, software-pipelined by one half.  Half h starts with
+  // S_h in one accumulator set, its maximum already applied:
+  //   at a tile boundary (h + 1 even): wait for tile (h + 1) / 2; barrier
+  //     (every wave is past the PV of tile (h + 1) / 2 - 2, whose stage is
+  //     free); issue tile (h + 1) / 2 + 2;
+  //   A: the 8 MFMAs of S_{h+1}  +  exp / pack / row sum of half h
+  //   B: the 8 MFMAs of PV_h     +  row maximum of S_{h+1};  lazy rescale.
+  // Each wave's vector work thus runs under its own matrix work.  The
+  // steady state runs in blocks of 8 halves (4 tiles, one turn of the stage
+  // ring) whose halves have no key past L, as straight-line code (a branch
+  // between the phases would let the compiler move the vector work out of
+  // the MFMA sequence); the remaining halves, the ragged one included, take a
+  // plain per-half path.  Tiles are counted from t_begin.
+  const int key_begin = t_begin * ATT_KT;
+  const int nh = 2 * nkt;
+  const int nh_full = (L - key_begin) / 32 < nh ? (L - key_begin) / 32 : nh;  // halves with no key past L
+  auto boundary = [&](int t, int stage_next2) __attribute__((always_inline)) {
+    // this wave's copies of tile t have landed; those of tile t + 1 may be in flight
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
+    __syncthreads();
+    issue_tile(t + 2, stage_next2);
+  };
+  auto fresh_max = [&](float(&m)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) m[b] = -INFINITY;
+  };
+  f32x16 s0[QB], s1[QB];
+  issue_tile(0, 0);
+  issue_tile(1, 1);
+  boundary(0, 2);
   {
-    // iteration t: tile t sits in stage t%3, tile t+1 is in flight
-    f32x16 sacc[2][QB];
-    auto iteration = [&](auto stage_c, int t) __attribute__((always_inline)) {
-      constexpr int ST = decltype(stage_c)::value;
-      constexpr int ST2 = (ST + 2) % ATT_NSTAGE;
-      // this wave's loads of tile t have landed (tile t+1, if any, may still be in flight)
-      if (t + 1 < nkt)
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
-      else
-        __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (t + 2 < nkt) issue_tile(t_begin + t + 2, ST2);
-      compute_s(std::integral_constant<int, ST>{}, sacc);
-      softmax_pv(std::integral_constant<int, ST>{}, sacc, (t_begin + t) * ATT_KT);
-    };
-    for (int t = 0; t < nkt; t += 3) {
-      iteration(std::integral_constant<int, 0>{}, t);
-      if (t + 1 >= nkt) break;
-      iteration(std::integral_constant<int, 1>{}, t + 1);
-      if (t + 2 >= nkt) break;
-      iteration(std::integral_constant<int, 2>{}, t + 2);
+    s_half(smem, 0, s0, [](int) {});
+    if (key_begin + 32 > L) mask_half(s0, key_begin);
+    float m[QB];
+    fresh_max(m);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) max_chunk(s0, c, m);
+    update_max(m);
+  }
+
+  // H = h % 8: tile h / 2 in stage H / 2, key block H % 2, S_h in set H % 2
+  auto half_step = [&](auto h_c, int h) __attribute__((always_inline)) {
+    constexpr int H = decltype(h_c)::value;
+    constexpr int ST = H / 2, KB = H % 2;
+    constexpr int HN = (H + 1) % 8, STN = HN / 2, KBN = HN % 2;
+    auto& sc = pick2<KB>(s0, s1);
+    auto& sn = pick2<1 - KB>(s0, s1);
+    bf16x8 pf[QB][2];
+    float neg_mc[QB], psum[QB], m[QB];
+    exp_begin(neg_mc, psum);
+    if constexpr (KBN == 0) boundary((h + 1) / 2, (STN + 2) % ATT_NSTAGE);
+    s_half(smem + STN * ATT_TILE_BYTES, KBN, sn,
+           [&](int i) __attribute__((always_inline)) { exp_chunk(sc, i, neg_mc, psum, pf); });
+    exp_end(psum);
+    fresh_max(m);
+    pv_half(smem + ST * ATT_TILE_BYTES, KB, pf,
+            [&](int i) __attribute__((always_inline)) { max_chunk(sn, i, m); });
+    update_max(m);
+  };
+  int h = 0;
+  for (; h + 8 < nh_full; h += 8) {
+    half_step(std::integral_constant<int, 0>{}, h);
+    half_step(std::integral_constant<int, 1>{}, h + 1);
+    half_step(std::integral_constant<int, 2>{}, h + 2);
+    half_step(std::integral_constant<int, 3>{}, h + 3);
+    half_step(std::integral_constant<int, 4>{}, h + 4);
+    half_step(std::integral_constant<int, 5>{}, h + 5);
+    half_step(std::integral_constant<int, 6>{}, h + 6);
+    half_step(std::integral_constant<int, 7>{}, h + 7);
+  }
+  // The remaining halves one at a time (S_h is in s0, tile h / 2 in stage 0).
+  for (; h < nh; ++h) {
+    bf16x8 pf[QB][2];
+    float neg_mc[QB], psum[QB];
+    exp_begin(neg_mc, psum);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) exp_chunk(s0, c, neg_mc, psum, pf);
+    exp_end(psum);
+    pv_half(smem + ((h / 2) % ATT_NSTAGE) * ATT_TILE_BYTES, h % 2, pf, [](int) {});
+    if (h + 1 < nh) {
+      const int hn = h + 1, stn = (hn / 2) % ATT_NSTAGE;
+      if (hn % 2 == 0) boundary(hn / 2, (stn + 2) % ATT_NSTAGE);
+      s_half(smem + stn * ATT_TILE_BYTES, hn % 2, s0, [](int) {});
+      const int keyh = key_begin + hn * 32;
+      if (keyh + 32 > L) mask_half(s0, keyh);
+      float m[QB];
+      fresh_max(m);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) max_chunk(s0, c, m);
+      update_max(m);
     }
   }
+  // drain the copies still in flight (re-copies past the last tile) before
+  // the LDS is reused or the workgroup ends
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
   if (part_o != nullptr) {
     // split workgroup: unnormalised output in the accumulator layout (for each
