@@ -21,6 +21,7 @@ import numpy as np
 from .configs import Workload
 
 STREAM_WEIGHTS, STREAM_BIAS, STREAM_MOD, STREAM_XREF, STREAM_DRIFT, STREAM_AUDIO = 1, 2, 3, 4, 5, 6
+STREAM_WAN, STREAM_CONTEXT = 7, 8
 
 
 def _rng(seed: int, stream: int, sub: int = 0) -> np.random.Generator:
@@ -228,3 +229,30 @@ def random_anchor_keys(T: int, seed: int) -> np.ndarray:
     """Uniform [0, 1) keys, one per segment: the random draw behind the Random
     anchor strategy (its k anchors are the k largest keys)."""
     return _rng(seed, 98).uniform(0.0, 1.0, size=T).astype(np.float32)
+
+
+def make_wan_block_weights(w: Workload, seed: int | None = None) -> dict:
+    """The plain block parameters plus the Wan-style extras: cross-attention
+    projections wqc, wkc, wvc, woc [D, D] and biases ~ N(0, 0.02); RMSNorm
+    weights gq, gk, gqc, gkc and the cross-attention LN scale g3 ~ N(1, 0.1);
+    the LN shift b3 ~ N(0, 0.02).  The extras are fp32 vectors on the device
+    (rounded to the storage dtype like the modulation)."""
+    seed = w.seed if seed is None else seed
+    out = make_block_weights(w, seed)
+    D = w.D
+    for i, k in enumerate(("wqc", "wkc", "wvc", "woc")):
+        out[k] = _normal_rows(seed, STREAM_WAN, i, (D, D), scale=0.02, dtype=w.dtype)
+    r = _rng(seed, STREAM_WAN, 10)
+    for k in ("bqc", "bkc", "bvc", "boc"):
+        out[k] = storage_round(0.02 * r.standard_normal(D, dtype=np.float32), w.dtype)
+    for k in ("gq", "gk", "gqc", "gkc", "g3"):
+        out[k] = storage_round((1.0 + 0.1 * r.standard_normal(D)).astype(np.float32), w.dtype)
+    out["b3"] = storage_round((0.02 * r.standard_normal(D)).astype(np.float32), w.dtype)
+    return out
+
+
+def make_context(w: Workload, Lc: int, seed: int | None = None, element: int = 0) -> np.ndarray:
+    """Context tokens [Lc, D] ~ N(0, 1) (text / audio embeddings after their
+    input projection), storage-rounded; `element` picks the batch element."""
+    seed = w.seed if seed is None else seed
+    return _normal_rows(seed, STREAM_CONTEXT, element, (Lc, w.D), dtype=w.dtype)
