@@ -260,6 +260,69 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w,
                        const void* x, const int32_t* idx, int32_t n_sel, float* y_sel,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* -------------------------------------------------------- Wan-style block */
+/*
+ * The block of echo_block_partial with the extras of the Wan2.2-S2V family the
+ * paper evaluates (Sec. 4), on the same restricted-query path (Sec. 3.3:
+ * queries, cross-attention and FFN for the selected tokens; keys and values of
+ * the self-attention from all tokens), for a batch of B elements that share
+ * the weights (B = 2: the conditional and unconditional halves of
+ * classifier-free guidance):
+ *   a   = LN(x) * (1 + scale1) + shift1                          all rows
+ *   q   = RoPE(RMSNorm(a[idx] Wq^T + bq) * gq)                   selected rows
+ *   k   = RoPE(RMSNorm(a Wk^T + bk) * gk);  v = a Wv^T + bv      all rows
+ *   x1  = x[idx] + gate1 * (attn(q, k, v) Wo^T + bo)
+ *   c   = LN(x1) * g3 + b3
+ *   qc  = RMSNorm(c Wqc^T + bqc) * gqc
+ *   kc  = RMSNorm(ctx Wkc^T + bkc) * gkc;  vc = ctx Wvc^T + bvc  all context rows
+ *   x2  = x1 + attn(qc, kc, vc) Woc^T + boc
+ *   y_sel = x2 + gate2 * (GELU_tanh(LN2(x2) W1^T + b1) W2^T + b2)
+ * RMSNorm(z) = z / sqrt(mean(z^2) + rms_eps) over all D channels.  RoPE: token
+ * i of the T x gh x gw latent grid sits at (t, r, c) = (i / (gh gw),
+ * (i / gw) % gh, i % gw); the dh/2 channel pairs (2j, 2j+1) of every head turn
+ * by t, r and c times base^(-j'/n) for the first dh/2 - 2(dh/6) pairs, the
+ * next dh/6 and the last dh/6 respectively (j' and n: the pair's index within
+ * its axis and the axis's pair count).  Attention as in echo_block_partial;
+ * the self-attention of element b sees the keys of element b only, the
+ * cross-attention the Lc context rows of element b.
+ * x [B][L][D] and ctx [B][Lc][D] in `dtype`; idx [sum n_sel] device int32:
+ * global rows b * L + i, element by element (the rows of element b are
+ * idx[o_b .. o_b + n_sel[b]) with o_b = n_sel[0] + .. + n_sel[b-1]), any order
+ * within an element; n_sel is a HOST array of B counts; y_sel [sum n_sel][D]
+ * fp32 in idx order.  Weights as in echo_block_weights, the cross-attention
+ * matrices [D][D] and biases [D] in `dtype`; gq, gk, gqc, gkc, g3, b3 fp32 [D].
+ * Supported: ECHO_BF16 with D/H == 128, D % 256 == 0, F % 256 == 0, T*gh*gw ==
+ * L, and B*L*D, B*Lc*D, sum(n_sel)*F each below 2^30 elements.
+ */
+typedef struct {
+  int32_t B;
+  int32_t L;
+  int32_t D;
+  int32_t H;
+  int32_t F;
+  int32_t Lc;          /* context rows per element */
+  int32_t T, gh, gw;   /* latent grid, T * gh * gw == L */
+  int32_t dtype;
+  float ln_eps;
+  float rms_eps;
+  double rope_base;    /* e.g. 10000 */
+  int32_t flags;       /* 0 or ECHO_BLOCK_BATCH_INVARIANT */
+} echo_wan_block_cfg;
+
+typedef struct {
+  echo_block_weights self;            /* modulation, self-attention and FFN */
+  const void* wqc; const void* wkc; const void* wvc; const void* woc;
+  const void* bqc; const void* bkc; const void* bvc; const void* boc;
+  const float* gq; const float* gk;   /* self-attention RMSNorm weights */
+  const float* gqc; const float* gkc; /* cross-attention RMSNorm weights */
+  const float* g3; const float* b3;   /* cross-attention LN scale and shift */
+} echo_wan_block_weights;
+
+size_t echo_wan_block_workspace(const echo_wan_block_cfg* cfg, int32_t n_total_max);
+int echo_wan_block_partial(const echo_wan_block_cfg* cfg, const echo_wan_block_weights* w, const void* x,
+                           const void* ctx, const int32_t* idx, const int32_t* n_sel, float* y_sel,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------- cache update */
 /*
  * Cache write and mask fusion (Sec. 3.3: out = m * fresh + (1 - m) * cached;

@@ -44,6 +44,19 @@ class BlockWeights(ctypes.Structure):
                                         "bq", "bk", "bv", "bo", "b1", "b2", "mod")]
 
 
+WAN_EXTRA = ("wqc", "wkc", "wvc", "woc", "bqc", "bkc", "bvc", "boc", "gq", "gk", "gqc", "gkc", "g3", "b3")
+
+
+class WanBlockCfg(ctypes.Structure):
+    _fields_ = [("B", c_int32), ("L", c_int32), ("D", c_int32), ("H", c_int32), ("F", c_int32),
+                ("Lc", c_int32), ("T", c_int32), ("gh", c_int32), ("gw", c_int32), ("dtype", c_int32),
+                ("ln_eps", c_float), ("rms_eps", c_float), ("rope_base", c_double), ("flags", c_int32)]
+
+
+class WanBlockWeights(ctypes.Structure):
+    _fields_ = [("self", BlockWeights)] + [(n, c_void_p) for n in WAN_EXTRA]
+
+
 class CacheCfg(ctypes.Structure):
     _fields_ = [("L", c_int32), ("D", c_int32), ("dtype", c_int32)]
 
@@ -95,6 +108,10 @@ _SIGNATURES = {
     "echo_block_workspace": (c_size_t, [_P(BlockCfg), c_int32]),
     "echo_block_partial": (ctypes.c_int, [_P(BlockCfg), _P(BlockWeights), c_void_p, c_void_p,
                                           c_int32, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "echo_wan_block_workspace": (c_size_t, [_P(WanBlockCfg), c_int32]),
+    "echo_wan_block_partial": (ctypes.c_int, [_P(WanBlockCfg), _P(WanBlockWeights), c_void_p, c_void_p,
+                                              c_void_p, _P(c_int32), c_void_p, c_void_p, c_size_t,
+                                              c_void_p]),
     "echo_cache_update": (ctypes.c_int, [_P(CacheCfg), c_void_p, c_void_p, c_void_p, c_int32,
                                          c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                          c_void_p]),

@@ -20,7 +20,8 @@ import math
 import torch
 
 from . import _lib
-from ._lib import (BlockCfg, BlockWeights, CacheCfg, EnergyCfg, KernelTime, RefCacheCfg,
+from ._lib import (BlockCfg, BlockWeights, CacheCfg, EnergyCfg, KernelTime, RefCacheCfg, WanBlockCfg,
+                   WanBlockWeights,
                    RefCacheState, ScheduleCfg, ScheduleState, SelectCfg,
                    ECHO_BF16, ECHO_F32, check)
 
@@ -401,6 +402,54 @@ def block_partial(params: dict, x: torch.Tensor, idx: torch.Tensor, n_sel: int, 
           lib.echo_block_partial(ctypes.byref(cfg), ctypes.byref(w), _ptr(x), _ptr(idx), n_sel,
                                  _ptr(y_sel), _ptr(ws), ws.numel(), _stream()))
     return y_sel[:n_sel]
+
+
+# ----------------------------------------------------------- Wan-style block
+
+def wan_block_partial(params: dict, x: torch.Tensor, ctx: torch.Tensor, idx: torch.Tensor, n_sel,
+                      H: int, grid, ln_eps: float = 1e-6, rms_eps: float = 1e-6, rope_base: float = 10000.0,
+                      y_sel: torch.Tensor | None = None, workspace: Workspace | None = None,
+                      batch_invariant: bool = False) -> torch.Tensor:
+    """echo_wan_block_partial: x [B, L, D], ctx [B, Lc, D] (bf16); idx int32 global
+    rows b * L + i, element by element; n_sel the B per-element counts (host
+    ints); grid (T, gh, gw).  Returns y_sel [sum(n_sel), D] fp32 in idx order.
+    params: the block weights plus wqc, wkc, wvc, woc, bqc, bkc, bvc, boc (in
+    x's dtype) and gq, gk, gqc, gkc, g3, b3 (fp32 [D])."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    _dev(ctx, "ctx", x.dtype)
+    B, L, D = x.shape
+    Lc = ctx.shape[1]
+    if ctx.shape[0] != B or ctx.shape[2] != D:
+        raise ValueError("ctx must be [B, Lc, D]")
+    counts = [int(v) for v in n_sel]
+    if len(counts) != B:
+        raise ValueError("n_sel needs one count per batch element")
+    tot = sum(counts)
+    F = params["w1"].shape[0]
+    for n in WEIGHT_NAMES[:-1] + ("wqc", "wkc", "wvc", "woc", "bqc", "bkc", "bvc", "boc"):
+        if params[n].dtype != x.dtype:
+            raise TypeError(f"{n} must have the activation dtype {x.dtype}")
+    for n in ("mod", "gq", "gk", "gqc", "gkc", "g3", "b3"):
+        _dev(params[n], n, torch.float32)
+    T_, gh, gw = (int(v) for v in grid)
+    cfg = WanBlockCfg(B, L, D, H, F, Lc, T_, gh, gw, _echo_dtype(x), float(ln_eps), float(rms_eps),
+                      float(rope_base), _lib.ECHO_BLOCK_BATCH_INVARIANT if batch_invariant else 0)
+    w = WanBlockWeights(block_weights(params), *[params[n].data_ptr() for n in _lib.WAN_EXTRA])
+    if y_sel is None:
+        y_sel = torch.empty((max(tot, 1), D), dtype=torch.float32, device=x.device)
+    if tot == 0:
+        return y_sel[:0]
+    _dev(idx, "idx", torch.int32)
+    need = lib.echo_wan_block_workspace(ctypes.byref(cfg), tot)
+    if need == 0:
+        check("echo_wan_block_partial", _lib.ECHO_EINVAL)
+    ws = (workspace or _WS["block"]).get(need, x.device)
+    arr = (ctypes.c_int32 * B)(*counts)
+    check("echo_wan_block_partial",
+          lib.echo_wan_block_partial(ctypes.byref(cfg), ctypes.byref(w), _ptr(x), _ptr(ctx), _ptr(idx), arr,
+                                     _ptr(y_sel), _ptr(ws), ws.numel(), _stream()))
+    return y_sel[:tot]
 
 
 # --------------------------------------------------------------- cache update

@@ -166,6 +166,72 @@ bool weights_ok(const echo_block_weights* w) {
 
 }  // namespace
 
+namespace {
+bool refcache_cfg_ok(const echo_refcache_cfg* c) {
+  return c != nullptr && c->L >= 1 && c->D >= 8 && (c->D % 8) == 0 && c->D <= 16384 && ok_dtype(c->dtype) &&
+         c->chain_len >= 1 && (c->L % c->chain_len) == 0 && std::isfinite(c->tau) &&
+         static_cast<int64_t>(c->capacity) >= static_cast<int64_t>(c->L) + c->L / c->chain_len;
+}
+bool refcache_state_ok(const echo_refcache_state* s) {
+  return s != nullptr && ok_ptr(s->pool) && ok_ptr(s->refcount) && ok_ptr(s->free_list) && ok_ptr(s->free_top) &&
+         ok_ptr(s->chain_ref) && ok_ptr(s->ent_slot) && ok_ptr(s->ent_kind) && ok_ptr(s->codes) &&
+         ok_ptr(s->scale);
+}
+}  // namespace
+
+namespace {
+bool wan_cfg_ok(const echo_wan_block_cfg* c) {
+  return c != nullptr && c->B >= 1 && c->L >= 1 && c->D >= 8 && c->H >= 1 && c->F >= 8 && c->Lc >= 1 &&
+         c->T >= 1 && c->gh >= 1 && c->gw >= 1 && int64_t(c->T) * c->gh * c->gw == c->L &&
+         ok_dtype(c->dtype) && c->D <= 16384 && c->F <= 65536 && (c->D % c->H) == 0 && (c->D % 8) == 0 &&
+         (c->F % 8) == 0 && c->ln_eps >= 0.0f && c->rms_eps >= 0.0f && std::isfinite(c->rope_base) &&
+         c->rope_base > 0.0 && (c->flags & ~ECHO_BLOCK_BATCH_INVARIANT) == 0;
+}
+bool wan_supported(const echo_wan_block_cfg* c) {
+  const int64_t lim = int64_t(1) << 30;
+  return c->dtype == ECHO_BF16 && c->D / c->H == 128 && (c->D % 256) == 0 && (c->F % 256) == 0 &&
+         int64_t(c->B) * c->L * c->D < lim && int64_t(c->B) * c->Lc * c->D < lim && int64_t(c->F) * c->D < lim;
+}
+struct WanWs {
+  void *a, *kv, *kvc, *q, *o, *b, *h;
+  float *x1, *x2, *part, *ones, *g3m1;
+  float2* tab;
+  size_t bytes;
+};
+WanWs wan_ws_layout(const echo_wan_block_cfg* c, int64_t n, char* base) {
+  const size_t es = esize(c->dtype);
+  const size_t BL = size_t(c->B) * c->L, BLc = size_t(c->B) * c->Lc, D = c->D, F = c->F, m = size_t(n);
+  WanWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* p = base ? base + off : nullptr;
+    off += align_up(bytes);
+    return p;
+  };
+  w.a = take(BL * D * es);
+  w.kv = take(BL * 2 * D * es);
+  w.kvc = take(BLc * 2 * D * es);
+  w.q = take(m * D * es);
+  w.o = take(m * D * es);
+  w.b = take(m * D * es);
+  w.h = take(m * F * es);
+  w.x1 = reinterpret_cast<float*>(take(m * D * 4));
+  w.x2 = reinterpret_cast<float*>(take(m * D * 4));
+  w.part = reinterpret_cast<float*>(take(block_partial_bytes()));
+  w.ones = reinterpret_cast<float*>(take(D * 4));
+  w.g3m1 = reinterpret_cast<float*>(take(D * 4));
+  w.tab = reinterpret_cast<float2*>(take(sizeof(float2) * size_t(rope_table_entries(c->T, c->gh, c->gw,
+                                                                                     c->D / c->H))));
+  w.bytes = off;
+  return w;
+}
+bool wan_weights_ok(const echo_wan_block_weights* w) {
+  return w != nullptr && weights_ok(&w->self) && ok_ptr(w->wqc) && ok_ptr(w->wkc) && ok_ptr(w->wvc) &&
+         ok_ptr(w->woc) && ok_ptr(w->bqc) && ok_ptr(w->bkc) && ok_ptr(w->bvc) && ok_ptr(w->boc) &&
+         ok_ptr(w->gq) && ok_ptr(w->gk) && ok_ptr(w->gqc) && ok_ptr(w->gkc) && ok_ptr(w->g3) && ok_ptr(w->b3);
+}
+}  // namespace
+
 extern "C" {
 
 const char* echo_status_str(int status) {
@@ -412,6 +478,118 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
   return ECHO_OK;
 }
 
+
+size_t echo_wan_block_workspace(const echo_wan_block_cfg* cfg, int32_t n_total_max) {
+  if (!wan_cfg_ok(cfg) || n_total_max < 0) return 0;
+  return wan_ws_layout(cfg, n_total_max, nullptr).bytes;
+}
+
+int echo_wan_block_partial(const echo_wan_block_cfg* cfg, const echo_wan_block_weights* w, const void* x,
+                           const void* ctx, const int32_t* idx, const int32_t* n_sel, float* y_sel,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  if (!wan_cfg_ok(cfg) || !wan_weights_ok(w) || n_sel == nullptr) return ECHO_EINVAL;
+  int64_t tot = 0;
+  for (int b = 0; b < cfg->B; ++b) {
+    if (n_sel[b] < 0 || n_sel[b] > cfg->L) return ECHO_EINVAL;
+    tot += n_sel[b];
+  }
+  if (!wan_supported(cfg)) return ECHO_EUNSUPPORTED;
+  if (tot == 0) return ECHO_OK;
+  if (tot * cfg->F >= (int64_t(1) << 30)) return ECHO_EUNSUPPORTED;
+  if (!ok_ptr(x) || !ok_ptr(ctx) || !ok_ptr(idx) || !ok_ptr(y_sel)) return ECHO_EINVAL;
+  const size_t need = wan_ws_layout(cfg, tot, nullptr).bytes;
+  if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
+  const WanWs ws = wan_ws_layout(cfg, tot, static_cast<char*>(workspace));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int B = cfg->B, L = cfg->L, D = cfg->D, H = cfg->H, F = cfg->F, Lc = cfg->Lc, n = static_cast<int>(tot);
+  const int BL = B * L, BLc = B * Lc, dh = D / H;
+  const float* mod = w->self.mod;
+  typedef const bf16_t* P;
+  float* part = (cfg->flags & ECHO_BLOCK_BATCH_INVARIANT) ? nullptr : ws.part;
+  auto with_part = [&](GemmBf16Args a) {
+    a.part = part;
+    a.part_bytes = block_partial_bytes();
+    return a;
+  };
+  hipError_t e;
+#define ECHO_TRY(call)                              \
+  if ((e = (call)) != hipSuccess) return device_status(e);
+  // constants: rotary table, the unit gate of the cross-attention output, g3 - 1
+  ECHO_TRY(launch_rope_table(cfg->T, cfg->gh, cfg->gw, dh, cfg->rope_base, ws.tab, st));
+  ECHO_TRY(launch_vec_shift(nullptr, 1.0f, ws.ones, D, st));
+  ECHO_TRY(launch_vec_shift(w->g3, -1.0f, ws.g3m1, D, st));
+  // self-attention
+  ECHO_TRY(launch_modln_input(1, x, BL, D, mod + 0 * D, mod + 1 * D, cfg->ln_eps, ws.a, st));
+  GemmBf16Args g{};
+  g = GemmBf16Args{static_cast<P>(ws.a), D, idx, BL, static_cast<P>(w->self.wq), static_cast<P>(w->self.wq), D, D,
+                   static_cast<P>(w->self.bq), static_cast<P>(w->self.bq), n, D, D, ws.q, D,
+                   nullptr, nullptr, 0, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_q_bf16", 0, with_part(g), st));
+  g = GemmBf16Args{static_cast<P>(ws.a), D, nullptr, BL, static_cast<P>(w->self.wk), static_cast<P>(w->self.wv), D,
+                   D, static_cast<P>(w->self.bk), static_cast<P>(w->self.bv), BL, 2 * D, D, ws.kv, 2 * D,
+                   nullptr, nullptr, 0, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_kv_bf16", 0, with_part(g), st));
+  ECHO_TRY(launch_qk_norm_rope(static_cast<bf16_t*>(ws.q), D, n, D, w->gq, cfg->rms_eps, idx, ws.tab, L, cfg->T,
+                               cfg->gh, cfg->gw, dh, st));
+  ECHO_TRY(launch_qk_norm_rope(static_cast<bf16_t*>(ws.kv), 2 * D, BL, D, w->gk, cfg->rms_eps, nullptr, ws.tab, L,
+                               cfg->T, cfg->gh, cfg->gw, dh, st));
+  {
+    const bf16_t* kvp = static_cast<const bf16_t*>(ws.kv);
+    int64_t o = 0;
+    for (int b = 0; b < B; ++b) {
+      const bf16_t* kb = kvp + int64_t(b) * L * 2 * D;
+      ECHO_TRY(launch_attn_bf16(static_cast<P>(ws.q) + o * D, D, kb, kb + D, 2 * D, n_sel[b], L, H,
+                                static_cast<bf16_t*>(ws.o) + o * D, D, part, block_partial_bytes(), st));
+      o += n_sel[b];
+    }
+  }
+  g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, n, static_cast<P>(w->self.wo), static_cast<P>(w->self.wo), D,
+                   D, static_cast<P>(w->self.bo), static_cast<P>(w->self.bo), n, D, D, ws.x1, D,
+                   mod + 2 * D, x, D, idx, 1};
+  ECHO_TRY(launch_gemm_bf16("gemm_o_bf16", 2, with_part(g), st));
+  // cross-attention: c = LN(x1) * g3 + b3 = LN(x1) * (1 + (g3 - 1)) + b3
+  ECHO_TRY(launch_modln_x1(1, ws.x1, n, D, w->b3, ws.g3m1, cfg->ln_eps, ws.b, st));
+  g = GemmBf16Args{static_cast<P>(ws.b), D, nullptr, n, static_cast<P>(w->wqc), static_cast<P>(w->wqc), D, D,
+                   static_cast<P>(w->bqc), static_cast<P>(w->bqc), n, D, D, ws.q, D,
+                   nullptr, nullptr, 0, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_qc_bf16", 0, with_part(g), st));
+  g = GemmBf16Args{static_cast<P>(ctx), D, nullptr, BLc, static_cast<P>(w->wkc), static_cast<P>(w->wvc), D, D,
+                   static_cast<P>(w->bkc), static_cast<P>(w->bvc), BLc, 2 * D, D, ws.kvc, 2 * D,
+                   nullptr, nullptr, 0, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_kvc_bf16", 0, with_part(g), st));
+  ECHO_TRY(launch_qk_norm_rope(static_cast<bf16_t*>(ws.q), D, n, D, w->gqc, cfg->rms_eps, nullptr, nullptr, L,
+                               cfg->T, cfg->gh, cfg->gw, dh, st));
+  ECHO_TRY(launch_qk_norm_rope(static_cast<bf16_t*>(ws.kvc), 2 * D, BLc, D, w->gkc, cfg->rms_eps, nullptr, nullptr,
+                               L, cfg->T, cfg->gh, cfg->gw, dh, st));
+  {
+    const bf16_t* kvp = static_cast<const bf16_t*>(ws.kvc);
+    int64_t o = 0;
+    for (int b = 0; b < B; ++b) {
+      const bf16_t* kb = kvp + int64_t(b) * Lc * 2 * D;
+      ECHO_TRY(launch_attn_bf16(static_cast<P>(ws.q) + o * D, D, kb, kb + D, 2 * D, n_sel[b], Lc, H,
+                                static_cast<bf16_t*>(ws.o) + o * D, D, part, block_partial_bytes(), st));
+      o += n_sel[b];
+    }
+  }
+  // x2 = x1 + 1 * (oc Woc^T + boc)
+  g = GemmBf16Args{static_cast<P>(ws.o), D, nullptr, n, static_cast<P>(w->woc), static_cast<P>(w->woc), D, D,
+                   static_cast<P>(w->boc), static_cast<P>(w->boc), n, D, D, ws.x2, D,
+                   ws.ones, ws.x1, D, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_oc_bf16", 2, with_part(g), st));
+  // FFN
+  ECHO_TRY(launch_modln_x1(1, ws.x2, n, D, mod + 3 * D, mod + 4 * D, cfg->ln_eps, ws.b, st));
+  g = GemmBf16Args{static_cast<P>(ws.b), D, nullptr, n, static_cast<P>(w->self.w1), static_cast<P>(w->self.w1), F,
+                   D, static_cast<P>(w->self.b1), static_cast<P>(w->self.b1), n, F, D, ws.h, F,
+                   nullptr, nullptr, 0, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_ffn_up_bf16", 1, with_part(g), st));
+  g = GemmBf16Args{static_cast<P>(ws.h), F, nullptr, n, static_cast<P>(w->self.w2), static_cast<P>(w->self.w2), D,
+                   F, static_cast<P>(w->self.b2), static_cast<P>(w->self.b2), n, D, F, y_sel, D,
+                   mod + 5 * D, ws.x2, D, nullptr, 0};
+  ECHO_TRY(launch_gemm_bf16("gemm_ffn_down_bf16", 2, with_part(g), st));
+#undef ECHO_TRY
+  return ECHO_OK;
+}
+
 int echo_cache_update(const echo_cache_cfg* cfg, const void* x, const int32_t* idx, const uint8_t* mask,
                       int32_t n_sel, const float* y_sel, void* xref, int8_t* codes, float* scale,
                       void* y, void* stream) {
@@ -443,18 +621,6 @@ int echo_cache_update_codec(const echo_cache_cfg* cfg, int32_t codec, const void
                                           y_sel, xref, store, codes, scale, y, static_cast<hipStream_t>(stream)));
 }
 
-namespace {
-bool refcache_cfg_ok(const echo_refcache_cfg* c) {
-  return c != nullptr && c->L >= 1 && c->D >= 8 && (c->D % 8) == 0 && c->D <= 16384 && ok_dtype(c->dtype) &&
-         c->chain_len >= 1 && (c->L % c->chain_len) == 0 && std::isfinite(c->tau) &&
-         static_cast<int64_t>(c->capacity) >= static_cast<int64_t>(c->L) + c->L / c->chain_len;
-}
-bool refcache_state_ok(const echo_refcache_state* s) {
-  return s != nullptr && ok_ptr(s->pool) && ok_ptr(s->refcount) && ok_ptr(s->free_list) && ok_ptr(s->free_top) &&
-         ok_ptr(s->chain_ref) && ok_ptr(s->ent_slot) && ok_ptr(s->ent_kind) && ok_ptr(s->codes) &&
-         ok_ptr(s->scale);
-}
-}  // namespace
 
 int echo_refcache_init(const echo_refcache_cfg* cfg, const echo_refcache_state* st, void* stream) {
   if (!refcache_cfg_ok(cfg) || !refcache_state_ok(st)) return ECHO_EINVAL;

@@ -99,6 +99,16 @@ hipError_t launch_refcache_update(int dtype_bf16, const void* x, const int32_t* 
                                   int32_t* chain_ref, int32_t* ent_slot, uint8_t* ent_kind, int8_t* codes,
                                   float* scale, void* xref, void* y, hipStream_t stream);
 
+// Wan-style block extras: rotary table ((cos, sin) per axis position and pair),
+// in-place qk RMSNorm (+ 3D RoPE when tab is not null) of M rows of z, and
+// out = (a ? a : 0) + beta
+int rope_table_entries(int T, int gh, int gw, int dh);
+hipError_t launch_rope_table(int T, int gh, int gw, int dh, double base, float2* tab, hipStream_t stream);
+hipError_t launch_qk_norm_rope(bf16_t* z, int64_t ldz, int M, int D, const float* g, float eps,
+                               const int32_t* rows, const float2* tab, int L, int T, int gh, int gw, int dh,
+                               hipStream_t stream);
+hipError_t launch_vec_shift(const float* a, float beta, float* out, int n, hipStream_t stream);
+
 hipError_t launch_modln_input(int dtype_bf16, const void* x, int M, int D, const float* shift,
                               const float* scale, float eps, void* out, hipStream_t stream);
 hipError_t launch_modln_x1(int dtype_bf16, const float* x1, int M, int D, const float* shift,

@@ -160,3 +160,30 @@ def test_cache_codec_rejects_before_launch(lib):
     assert run(_lib.ECHO_CODEC_RESIDUAL_INT8, scale=MISALIGNED) == _lib.ECHO_EINVAL
     assert run(_lib.ECHO_CODEC_FULL, cfg=_lib.CacheCfg(32, 60, 1)) == _lib.ECHO_EINVAL
     assert run(_lib.ECHO_CODEC_FULL, n=33) == _lib.ECHO_EINVAL
+
+
+def test_wan_block_rejects_before_launch(lib):
+    w = _lib.WanBlockWeights(_lib.BlockWeights(*([0x20000] * 13)), *([0x20000] * 14))
+    counts = (ctypes.c_int32 * 2)(10, 12)
+
+    def run(cfg, weights=w, n=counts, x=FAKE):
+        return lib.echo_wan_block_partial(ctypes.byref(cfg), ctypes.byref(weights), x, FAKE, FAKE, n, FAKE,
+                                          FAKE, 1 << 40, None)
+
+    def cfg(**kw):
+        base = dict(B=2, L=300, D=256, H=2, F=512, Lc=77, T=3, gh=10, gw=10, dtype=1, ln_eps=1e-6,
+                    rms_eps=1e-6, rope_base=1e4, flags=0)
+        base.update(kw)
+        return _lib.WanBlockCfg(**base)
+    assert run(cfg(gw=11)) == _lib.ECHO_EINVAL                     # T * gh * gw != L
+    assert run(cfg(Lc=0)) == _lib.ECHO_EINVAL
+    assert run(cfg(rope_base=float("nan"))) == _lib.ECHO_EINVAL
+    assert run(cfg(flags=2)) == _lib.ECHO_EINVAL
+    assert run(cfg(dtype=0)) == _lib.ECHO_EUNSUPPORTED              # bf16 only
+    assert run(cfg(D=192, H=2)) == _lib.ECHO_EUNSUPPORTED           # head width 96
+    assert run(cfg(), n=(ctypes.c_int32 * 2)(10, 301)) == _lib.ECHO_EINVAL
+    assert run(cfg(), x=MISALIGNED) == _lib.ECHO_EINVAL
+    bad = _lib.WanBlockWeights(_lib.BlockWeights(*([0x20000] * 13)), *([0x20000] * 13 + [0]))   # null b3
+    assert run(cfg(), weights=bad) == _lib.ECHO_EINVAL
+    assert lib.echo_wan_block_workspace(ctypes.byref(cfg()), 100) > 0
+    assert lib.echo_wan_block_workspace(ctypes.byref(cfg(T=2)), 100) == 0
