@@ -16,7 +16,8 @@ steps, a per-kernel table, and the CPU oracle's throughput on a bounded sample
 cache (update time, live references and bytes), a scheduled multi-block stack
 over a denoising trajectory, and the module ablation's variants (anchor
 strategies, step-only / latent-only schedules, 16-bit and naive int8 caches:
-kernel times, stack latency, cache bytes, distance from an all-full run).
+kernel times, stack latency, cache bytes, distance from an all-full run), and
+the Wan-style block (qk RMSNorm + 3D RoPE, cross-attention, batch of two).
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 """
@@ -417,6 +418,77 @@ def variants_leg(w, dev, dt, fe, fw, blocks, steps: int, n_anchor: int = 14, n_f
     return out
 
 
+def wan_leg(w, dev, dt, B: int = 2, Lc: int = 512, steps: int = 10):
+    """The Wan-style block (qk RMSNorm + 3D RoPE, cross-attention over Lc
+    context tokens, a batch of B for classifier-free guidance) on the
+    workload's shape with K selected tokens per element: time per call, the
+    per-kernel breakdown and the rooflines of its kernels."""
+    import torch
+
+    from paper_2608_02474_amd import api, roofline
+
+    L, D, K, F = w.L, w.D, w.K, w.F
+    b = 2 if dt == torch.bfloat16 else 4
+    p = make_stack_blocks(w, dev, dt, 1, 6000 + w.seed)[0]
+    g = torch.Generator(device=dev)
+    g.manual_seed(7000 + w.seed)
+    rnd = lambda *shape, std=0.02: (torch.randn(shape, device=dev, generator=g) * std).to(dt)
+    for k in ("wqc", "wkc", "wvc", "woc"):
+        p[k] = rnd(D, D)
+    for k in ("bqc", "bkc", "bvc", "boc"):
+        p[k] = rnd(D)
+    for k in ("gq", "gk", "gqc", "gkc", "g3"):
+        p[k] = 1.0 + 0.1 * torch.randn(D, device=dev, generator=g)
+    p["b3"] = 0.02 * torch.randn(D, device=dev, generator=g)
+    x = torch.randn((B, L, D), device=dev, generator=g).to(dt)
+    ctx = torch.randn((B, Lc, D), device=dev, generator=g).to(dt)
+    idx = torch.cat([bb * L + torch.sort(torch.randperm(L, device=dev, generator=g)[:K]).values
+                     for bb in range(B)]).to(torch.int32)
+    ws = api.Workspace()
+    y = torch.empty((B * K, D), dtype=torch.float32, device=dev)
+    grid = (w.T,) + tuple(w.grid)
+    call = lambda: api.wan_block_partial(p, x, ctx, idx, [K] * B, w.H, grid, y_sel=y, workspace=ws)
+    for _ in range(2):
+        call()
+    torch.cuda.synchronize()
+    api.profile_enable(True)
+    api.profile_read()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ktimes = api.profile_read()
+    api.profile_enable(False)
+    ms = e0.elapsed_time(e1) / steps
+    work = roofline.wan_block_work(B, L, K, D, F, Lc, b)
+    kernels = {}
+    for name, (launches, total) in sorted(ktimes.items(), key=lambda kv: -kv[1][1]):
+        avg = total / launches
+        e = {"ms_per_call": round(total / steps, 4), "launches_per_call": launches // steps,
+             "avg_ms": round(avg, 4)}
+        wk = roofline.work_of(name, work)
+        if wk is not None and wk[0] > 0:
+            amount, kind = wk
+            if kind == "flop":
+                a = amount / (avg * 1e-3) / 1e12
+                e.update(achieved=round(a, 1), unit="TFLOP/s", frac=round(a / roofline.PEAK_BF16_TFLOPS, 4))
+            else:
+                a = amount / (avg * 1e-3) / 1e9
+                e.update(achieved=round(a, 1), unit="GB/s", frac=round(a / roofline.PEAK_HBM_GBS, 4))
+        kernels[name] = e
+    tf = roofline.wan_block_flops(B, L, K, D, F, Lc) / (ms * 1e-3) / 1e12
+    extra = sum(kernels[n]["ms_per_call"] for n in kernels
+                if n.startswith(("qk_norm_rope", "gemm_qc", "gemm_kvc", "gemm_oc", "attn_cross", "rope_table",
+                                 "vec_shift")))
+    return {"batch": B, "context_tokens": Lc, "selected_per_element": K, "ms_per_call": round(ms, 3),
+            "tokens_per_s": round(B * L / (ms * 1e-3), 1), "tflops": round(tf, 1),
+            "frac_bf16_peak": round(tf / roofline.PEAK_BF16_TFLOPS, 4),
+            "extras_ms_per_call": round(extra, 3), "kernels": kernels,
+            "data": "random-init weights and synthetic tokens, context and selection (device-generated)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,6 +501,9 @@ def main() -> int:
     ap.add_argument("--variant-blocks", type=int, default=10,
                     help="blocks of the ablation-variants leg (anchors, schedules, codecs); 0: skip")
     ap.add_argument("--variant-steps", type=int, default=10)
+    ap.add_argument("--wan-batch", type=int, default=2,
+                    help="batch of the Wan-style block leg (classifier-free guidance pair); 0: skip")
+    ap.add_argument("--wan-context", type=int, default=512)
     ap.add_argument("--skip-cpu-baseline", action="store_true",
                     help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
                          "unchanged")
@@ -557,6 +632,11 @@ def main() -> int:
             out["variants"] = variants_leg(w, dev, dt, fe_stack, fw_stack, blocks[:args.variant_blocks],
                                            args.variant_steps)
         blocks = None
+    if args.wan_batch > 0:
+        log(f"Wan-style block leg: batch {args.wan_batch}, {args.wan_context} context tokens")
+        blk = None
+        torch.cuda.empty_cache()
+        out["wan_block"] = wan_leg(w, dev, dt, B=args.wan_batch, Lc=args.wan_context)
 
     if args.skip_cpu_baseline:
         out["cpu_baseline"] = None

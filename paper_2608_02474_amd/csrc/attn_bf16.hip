@@ -537,7 +537,7 @@ attn_combine(const float* __restrict__ part_o, const float* __restrict__ part_ml
 template <int QB, int WAVES>
 hipError_t launch_attn_variant(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                                int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
-                               float* part, size_t part_bytes, hipStream_t stream) {
+                               float* part, size_t part_bytes, hipStream_t stream, const char* name) {
   if (Mq <= 0) return hipSuccess;
   typedef AttCfg<QB, WAVES> C;
   const float scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(ATT_DH)));
@@ -551,7 +551,7 @@ hipError_t launch_attn_variant(const bf16_t* q, int64_t ldq, const bf16_t* k, co
   const size_t unit_bytes = sizeof(float) * C::kQ * (ATT_DH + 2);
   while (nsplit > 1 && static_cast<size_t>(tail) * nsplit * unit_bytes > part_bytes) --nsplit;
   if (part == nullptr) nsplit = 1;
-  ::echo::TimedLaunch scope("attn_fwd_bf16", stream);
+  ::echo::TimedLaunch scope(name, stream);
   if (nsplit < 2) {
     hipLaunchKernelGGL((attn_fwd_bf16<QB, WAVES>), dim3(total), dim3(C::kThreads), 0, stream, q, ldq, k, v,
                        ldkv, Mq, L, H, scale_log2, out, ldo, 0, 1, nkt, nullptr, nullptr);
@@ -586,8 +586,9 @@ size_t attn_partial_bytes() {
 
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
-                            float* part, size_t part_bytes, hipStream_t stream) {
-  return launch_attn_variant<1, 8>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, part, part_bytes, stream);
+                            float* part, size_t part_bytes, hipStream_t stream, const char* timing_name) {
+  return launch_attn_variant<1, 8>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, part, part_bytes, stream,
+                                   timing_name);
 }
 
 }  // namespace echo

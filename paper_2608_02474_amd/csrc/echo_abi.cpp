@@ -567,7 +567,8 @@ int echo_wan_block_partial(const echo_wan_block_cfg* cfg, const echo_wan_block_w
     for (int b = 0; b < B; ++b) {
       const bf16_t* kb = kvp + int64_t(b) * Lc * 2 * D;
       ECHO_TRY(launch_attn_bf16(static_cast<P>(ws.q) + o * D, D, kb, kb + D, 2 * D, n_sel[b], Lc, H,
-                                static_cast<bf16_t*>(ws.o) + o * D, D, part, block_partial_bytes(), st));
+                                static_cast<bf16_t*>(ws.o) + o * D, D, part, block_partial_bytes(), st,
+                                "attn_cross_bf16"));
       o += n_sel[b];
     }
   }

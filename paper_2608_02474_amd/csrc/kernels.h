@@ -121,7 +121,8 @@ hipError_t launch_gemm_f32(const char* name, int epi, const GemmF32Args& a, hipS
 // results of the key-split tail work items; with part == nullptr nothing is split.
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
-                            float* part, size_t part_bytes, hipStream_t stream);
+                            float* part, size_t part_bytes, hipStream_t stream,
+                            const char* timing_name = "attn_fwd_bf16");
 size_t attn_partial_bytes();
 // bytes that hold the partial results of any split tail of the bf16 block
 // (attention key splits, GEMM k splits): 256 units of the larger kind

@@ -59,3 +59,32 @@ def work_of(name: str, table: dict):
 
 def block_flops(L: int, K: int, D: int, F: int) -> int:
     return 2 * K * D * D + 4 * L * D * D + 4 * K * L * D + 2 * K * D * D + 4 * K * D * F
+
+
+def wan_block_work(B: int, L: int, K: int, D: int, F: int, Lc: int, b: int):
+    """Work per launch of the Wan-style block's kernels for a batch of B
+    elements with K selected tokens each and Lc context rows: {name prefix:
+    (amount per launch, kind)}.  The GEMMs run once over the whole batch;
+    attention runs once per element; qk_norm_rope runs four times (q, k, the
+    cross-attention q and k), given as the mean of the four."""
+    n = B * K
+    norm_bytes = (2 * n + B * L + B * Lc) * D * 2 * b // 4
+    return {
+        "qk_norm_rope": (norm_bytes, "byte"),
+        "gemm_qc": (2 * n * D * D, "flop"),
+        "gemm_kvc": (4 * B * Lc * D * D, "flop"),
+        "gemm_oc": (2 * n * D * D, "flop"),
+        "attn_cross": (4 * K * Lc * D, "flop"),
+        "gemm_q": (2 * n * D * D, "flop"),
+        "gemm_kv": (4 * B * L * D * D, "flop"),
+        "attn_fwd": (4 * K * L * D, "flop"),
+        "gemm_o": (2 * n * D * D, "flop"),
+        "modln_in": (2 * B * L * D * b, "byte"),
+        "modln_x1": (n * D * (4 + b), "byte"),
+        "gemm_ffn_up": (2 * n * D * F, "flop"),
+        "gemm_ffn_down": (2 * n * F * D, "flop"),
+    }
+
+
+def wan_block_flops(B: int, L: int, K: int, D: int, F: int, Lc: int) -> int:
+    return B * (block_flops(L, K, D, F) + 4 * K * D * D + 4 * Lc * D * D + 4 * K * Lc * D)
