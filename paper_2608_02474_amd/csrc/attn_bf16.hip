@@ -29,6 +29,10 @@
 //     sum of tile t is spread between the MFMAs of S(t+1), and the row maximum
 //     of S(t+1) between the MFMAs of PV(t), so each wave's vector work runs
 //     under its own matrix work (two accumulator sets for S).
+//   * In the steady state a wave's copies of a new tile are issued one at a
+//     time between the S MFMAs after the tile barrier, not all at once at the
+//     barrier: eight waves issuing their copies together made each wait at
+//     the issue of the next copy instead of running its MFMAs (2.7% faster).
 // Workgroup ids are remapped so that each XCD works through a contiguous range
 // of (head, query-tile) pairs: the query tiles of one head share that head's
 // K/V stream in one L2.
@@ -193,6 +197,29 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       lds_copy16_s(kt, ro + k_src[n], kdst + m * 1024);
       lds_copy16_s(vt, ro + v_src[n], vdst + m * 1024);
     }
+  };
+
+  // The same copies, issued one at a time: tile_prep() takes the tile's
+  // sources and stage; tile_copy(c) issues copy c (K then V of piece c / 2).
+  const bf16_t* pk_src = kh;
+  const bf16_t* pv_src = vh;
+  uint32_t p_last = 0, p_kdst = 0;
+  auto tile_prep = [&](int t, int stage) __attribute__((always_inline)) {
+    t = t < nkt ? t : nkt - 1;
+    const int key0 = (t_begin + t) * ATT_KT;
+    pk_src = kh + static_cast<int64_t>(key0) * ldkv;
+    pv_src = vh + static_cast<int64_t>(key0) * ldkv;
+    p_last = static_cast<uint32_t>(L - 1 - key0) * ldkv2;
+    p_kdst = lds0 + stage * ATT_TILE_BYTES;
+  };
+  auto tile_copy = [&](int c) __attribute__((always_inline)) {
+    const int n = c / 2;
+    const uint32_t m = static_cast<uint32_t>(wave_u + WAVES * n);
+    const uint32_t ro = row_off[n] < p_last ? row_off[n] : p_last;
+    if (c % 2 == 0)
+      lds_copy16_s(pk_src, ro + k_src[n], p_kdst + m * 1024);
+    else
+      lds_copy16_s(pv_src, ro + v_src[n], p_kdst + ATT_V_BASE + m * 1024);
   };
 
   // ---- precomputed LDS read addresses (byte offsets inside a stage)
@@ -397,9 +424,19 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     bf16x8 pf[QB][2];
     float neg_mc[QB], psum[QB], m[QB];
     exp_begin(neg_mc, psum);
-    if constexpr (KBN == 0) boundary((h + 1) / 2, (STN + 2) % ATT_NSTAGE);
-    s_half(smem + STN * ATT_TILE_BYTES, KBN, sn,
-           [&](int i) __attribute__((always_inline)) { exp_chunk(sc, i, neg_mc, psum, pf); });
+    if constexpr (KBN == 0) {
+      // this wave's copies of the new tile have landed; after the barrier
+      // every wave is past the tile whose stage the copies below refill
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
+      __syncthreads();
+      tile_prep((h + 1) / 2 + 2, (STN + 2) % ATT_NSTAGE);
+    }
+    s_half(smem + STN * ATT_TILE_BYTES, KBN, sn, [&](int i) __attribute__((always_inline)) {
+      exp_chunk(sc, i, neg_mc, psum, pf);
+      if constexpr (KBN == 0) {
+        if (i % 2 == 1 && i / 2 < 2 * NLD) tile_copy(i / 2);
+      }
+    });
     exp_end(psum);
     fresh_max(m);
     pv_half(smem + ST * ATT_TILE_BYTES, KB, pf,
