@@ -16,8 +16,12 @@ steps, a per-kernel table, and the CPU oracle's throughput on a bounded sample
 cache (update time, live references and bytes), a scheduled multi-block stack
 over a denoising trajectory, and the module ablation's variants (anchor
 strategies, step-only / latent-only schedules, 16-bit and naive int8 caches:
-kernel times, stack latency, cache bytes, distance from an all-full run), and
-the Wan-style block (qk RMSNorm + 3D RoPE, cross-attention, batch of two).
+kernel times, stack latency, cache bytes, distance from an all-full run),
+the Wan-style block (qk RMSNorm + 3D RoPE, cross-attention, batch of two), the
+streaming kernels timed alone after a read sweep that leaves the MALL clean,
+the 32760-token step swept over recompute ratios 0.1 / 0.25 / 0.5 / 1.0 under
+three audio energy profiles, and the 720p-shaped step (75600 tokens) with its
+cache footprint.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 """
@@ -536,6 +540,103 @@ def hbm_isolated_leg(blk, X, fw, w, dev, iters: int = 20):
             "kernels": out}
 
 
+def _timed_steps(step, steps: int, warmup: int = 2):
+    """ms per call of step() over `steps` calls (HIP events on the current
+    stream), plus the library's per-kernel record of those calls."""
+    import torch
+
+    from paper_2608_02474_amd import api
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    api.profile_enable(True)
+    api.profile_read()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    kt = api.profile_read()
+    api.profile_enable(False)
+    return start.elapsed_time(stop) / steps, kt
+
+
+def _block_frac(kt, steps, L, K, D, F):
+    from paper_2608_02474_amd import roofline
+
+    block_ms = sum(v[1] for n, v in kt.items() if n.startswith(("modln", "gemm_", "attn_fwd"))) / steps
+    tf = roofline.block_flops(L, K, D, F) / (block_ms * 1e-3) / 1e12
+    return round(block_ms, 4), round(tf / roofline.PEAK_BF16_TFLOPS, 4)
+
+
+def sweep_leg(w, blk, X, dev, steps: int = 10):
+    """The 32760-token block swept over the recompute ratio (1.0 recomputes
+    every token: the full block) under the three audio energy profiles of the
+    sweep; the whole step (energy, selection, partial block, cache update) is
+    timed, as in the main measurement."""
+    import torch
+
+    import synth
+    from paper_2608_02474_amd import api
+
+    out = {"ratios": list(synth.SWEEP_RATIOS), "profiles": {}}
+    for prof in synth.SWEEP_AUDIO:
+        A = torch.from_numpy(synth.make_audio(prof, w.n_samples, w.sample_rate, w.seed)).to(dev)
+        res = {}
+        for r in synth.SWEEP_RATIOS:
+            K = api.topk_count(r, w.L)
+
+            def step():
+                _, _, fw = api.energy(A, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
+                return blk.step(X, fw, w.N, k=K)
+            ms, kt = _timed_steps(step, steps)
+            bms, frac = _block_frac(kt, steps, w.L, K, w.D, w.F)
+            res[str(r)] = {"K": K, "ms_per_step": round(ms, 4), "tokens_per_s": round(w.L / (ms * 1e-3), 1),
+                           "recomputed_tokens_per_s": round(K / (ms * 1e-3), 1),
+                           "block_partial_ms": bms, "block_frac_bf16_peak": frac}
+        out["profiles"][prof] = res
+    return out
+
+
+def p720_leg(dev, dt, steps: int = 10):
+    """The 720p-shaped block (21 x 45 x 80 = 75600 tokens, ratio 0.3): whole-step
+    tokens/s and the cache footprint (int8 codes, fp32 scales, the bf16 reference)."""
+    import torch
+
+    import synth
+    from paper_2608_02474_amd import api
+
+    w = synth.WAN14B_720P
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    audio = synth.make_audio(w.audio, w.n_samples, w.sample_rate, w.seed)
+    P = {k: torch.from_numpy(v).to(torch.float32 if k == "mod" else dt).to(dev) for k, v in p.items()}
+    X = torch.from_numpy(x).to(dt).to(dev)
+    XR = torch.from_numpy(xref).to(dt).to(dev)
+    A = torch.from_numpy(audio).to(dev)
+    del p, x, xref
+    blk = api.CachedBlock(P, w.H, w.L, w.D, dev, dt)
+    blk.init(XR)
+    torch.cuda.synchronize()
+
+    def step():
+        _, _, fw = api.energy(A, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)
+        return blk.step(X, fw, w.N, k=w.K)
+    ms, kt = _timed_steps(step, steps)
+    bms, frac = _block_frac(kt, steps, w.L, w.K, w.D, w.F)
+    b = 2 if dt == torch.bfloat16 else 4
+    codes, scale, ref = w.L * w.D, 4 * w.L, w.L * w.D * b
+    return {"workload": w.name, "tokens": w.L, "recomputed_tokens": w.K, "ratio": w.ratio,
+            "ms_per_step": round(ms, 4), "tokens_per_s": round(w.L / (ms * 1e-3), 1),
+            "recomputed_tokens_per_s": round(w.K / (ms * 1e-3), 1),
+            "block_partial_ms": bms, "block_frac_bf16_peak": frac,
+            "cache_bytes": {"codes_int8": codes, "scale_fp32": scale, "reference": ref,
+                            "total": codes + scale + ref, "bf16_output_cache_for_comparison": w.L * w.D * 2},
+            "data": "synthetic (seeded; 720p-shaped latents, random-init block weights, speech-like audio)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -551,6 +652,10 @@ def main() -> int:
     ap.add_argument("--wan-batch", type=int, default=2,
                     help="batch of the Wan-style block leg (classifier-free guidance pair); 0: skip")
     ap.add_argument("--wan-context", type=int, default=512)
+    ap.add_argument("--sweep-steps", type=int, default=10,
+                    help="timed steps per (ratio, audio profile) of the ratio-sweep leg; 0: skip")
+    ap.add_argument("--p720-steps", type=int, default=10,
+                    help="timed steps of the 720p-shaped block leg; 0: skip")
     ap.add_argument("--skip-cpu-baseline", action="store_true",
                     help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
                          "unchanged")
@@ -671,6 +776,10 @@ def main() -> int:
     out["select_hbm_frac_isolated"] = out["hbm_isolated"]["kernels"].get("saliency_rows_bf16", {}).get("frac")
     out["cache_hbm_frac_isolated"] = out["hbm_isolated"]["kernels"].get("cache_update_bf16", {}).get("frac")
 
+    if args.sweep_steps > 0 and w.name == "wan14b_480p_32760tok":
+        log("ratio sweep leg: ratios x audio profiles")
+        out["ratio_sweep"] = sweep_leg(w, blk, X, dev, args.sweep_steps)
+
     log("adaptive reference cache leg")
     out["refcache"] = refcache_leg(w, dev, dt)
     if args.stack_blocks > 0 or args.variant_blocks > 0:
@@ -691,6 +800,13 @@ def main() -> int:
         blk = None
         torch.cuda.empty_cache()
         out["wan_block"] = wan_leg(w, dev, dt, B=args.wan_batch, Lc=args.wan_context)
+
+    if args.p720_steps > 0 and w.name != "wan14b_720p_75600tok":
+        log("720p-shaped block leg")
+        blk = None
+        torch.cuda.empty_cache()
+        out["p720"] = p720_leg(dev, dt, args.p720_steps)
+        torch.cuda.empty_cache()
 
     if args.skip_cpu_baseline:
         out["cpu_baseline"] = None

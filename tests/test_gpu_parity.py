@@ -233,6 +233,18 @@ def test_block_gates_one_informational():
     assert err.max() < 0.1
 
 
+_KV = {}
+
+
+def _kv_shared(w, p, x):
+    """The oracle's all-row LN + K/V projection of x, kept for the ratio cases
+    of one workload (it does not depend on the selection)."""
+    if w.name not in _KV:
+        _KV.clear()
+        _KV[w.name] = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    return _KV[w.name]
+
+
 @pytest.mark.parametrize("w", [synth.WAN14B_480P, synth.WAN14B_720P], ids=lambda w: w.name)
 def test_block_partial_full_size_sampled(w):
     """Full-size block in the launch configuration the benchmark times; the
@@ -248,8 +260,30 @@ def test_block_partial_full_size_sampled(w):
     rows = np.unique(np.concatenate([[0, w.K - 1, w.K // 2],
                                      rng.choice(w.K, 29, replace=False)]))
     say(f"block {w.name}: oracle on {len(rows)} sampled rows")
-    want = OB.block_partial(p, x, idx[rows], w.H)
+    kv = _kv_shared(w, p, x) if w is synth.WAN14B_480P else None
+    want = OB.block_partial(p, x, idx[rows], w.H, kv=kv)
     check_block(got[rows], want, w.dtype, f"{w.name}/sampled")
+
+
+@pytest.mark.parametrize("ratio", synth.SWEEP_RATIOS, ids=lambda r: f"r{r}")
+def test_block_partial_ratio_sweep_sampled(ratio):
+    """The 32760-token block at every recompute ratio of the sweep (K from
+    3276 to all 32760 tokens: other GEMM and attention grids and split tails
+    than the 0.4 case), sampled rows against the oracle."""
+    w = synth.WAN14B_480P.with_(ratio=ratio)
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w)
+    s, _, _ = OS.saliency(x, xref, fw, w.N)
+    idx = OS.select_topk(s, w.K)
+    say(f"block {w.name} r={ratio} K={w.K} (GPU)")
+    got = _block_gpu(w, p, x, idx)
+    rng = np.random.default_rng(10)
+    rows = np.unique(np.concatenate([[0, w.K - 1, w.K // 2],
+                                     rng.choice(w.K, 21, replace=False)]))
+    say(f"block r={ratio}: oracle on {len(rows)} sampled rows")
+    want = OB.block_partial(p, x, idx[rows], w.H, kv=_kv_shared(w, p, x))
+    check_block(got[rows], want, w.dtype, f"{w.name}/r{ratio}/sampled")
 
 
 def test_block_row_independence_full_size():
