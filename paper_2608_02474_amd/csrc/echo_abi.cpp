@@ -98,8 +98,9 @@ bool energy_cfg_ok(const echo_energy_cfg* c, int64_t n_samples) {
 }
 size_t energy_ws(const echo_energy_cfg* c, int64_t n_samples) {
   const int mf = energy_max_frames(n_samples, c->T, c->n_fft, c->hop);
+  // per-frame band energies, then per-segment energies and band sums
   return align_up(sizeof(double) * static_cast<size_t>(c->T) * mf * c->n_bands) +
-         align_up(sizeof(double) * static_cast<size_t>(c->T));
+         align_up(sizeof(double) * static_cast<size_t>(c->T) * (1 + c->n_bands));
 }
 
 // ---- select

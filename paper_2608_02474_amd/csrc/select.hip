@@ -10,9 +10,10 @@
 // select_rows: one 1024-thread workgroup, the keys held in registers
 //   (1) top-K threshold key by 4-pass 8-bit radix select over order-preserving
 //       uint32 keys (histograms in LDS);
-//   (2) stable compaction in index order: wave ballot + popcount gives each
-//       lane's rank among equal-key tokens and its output slot; ties at the
-//       threshold key go to the lowest indices.
+//   (2) stable compaction in index order: per (1024-key round, wave) counts,
+//       two block-wide exclusive scans (ranks of equal keys, output slots),
+//       then wave ballot + popcount within each wave; ties at the threshold
+//       key go to the lowest indices.
 // The key set is tiny (4 bytes per token, L2-resident), so one workgroup keeps
 // the selection exact and deterministic at a cost of a few microseconds.
 // select_segments: the same selection per anchor segment, one workgroup per
@@ -135,7 +136,6 @@ __device__ __forceinline__ void topk_rows(const float* __restrict__ s, int L, in
                                           uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sh_digit, sh_above;
-  __shared__ uint32_t wcnt[2][kSelWaves];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const uint64_t lt_mask = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
 
@@ -236,45 +236,90 @@ __device__ __forceinline__ void topk_rows(const float* __restrict__ s, int L, in
     take_eq = true;
   }
 
-  // (2) stable compaction in index order
-  uint32_t base_eq = 0, base_sel = 0;
+  // (2) stable compaction in index order, in chunks of CH rounds.  Round r,
+  //     wave w holds the indices r * 1024 + 64 w + lane, so the (r, w) pairs
+  //     taken round-major are in index order.  Per chunk:
+  //   a. every wave counts its keys above (gt) and equal to (eq) the
+  //      threshold key in each round;
+  //   b. one thread per (r, w): an exclusive scan of the eq counts gives the
+  //      rank of the pair's first equal key; the equal keys taken are those
+  //      ranked below need_eq, so the pair takes gt + clamp(need_eq - rank,
+  //      0, eq) keys; an exclusive scan of those gives its first output slot;
+  //   c. every lane writes its mask byte and, if taken, its index.
+  //   A handful of barriers per chunk instead of three per round.
+  constexpr int CH = kSelThreads / kSelWaves;  // 64 rounds: one (r, w) pair per thread in b
+  __shared__ uint32_t c_eq[CH * kSelWaves], c_sel[CH * kSelWaves];
+  __shared__ uint32_t s_tot[kSelWaves];
+  auto for_rounds = [&](int r0, auto&& body) __attribute__((always_inline)) {
+    if constexpr (R > 0) {
 #pragma unroll
-  for (int r = 0; r < (R > 0 ? R : 1); ++r) {
-    for (int rr = (R > 0 ? r : 0); rr < (R > 0 ? r + 1 : nr); ++rr) {
-      const int i = rr * kSelThreads + tid;
+      for (int r = 0; r < R; ++r)
+        if (r >= r0 && r < r0 + CH) body(r, kr[r]);
+    } else {
+      const int r1 = r0 + CH < nr ? r0 + CH : nr;
+      for (int r = r0; r < r1; ++r) body(r, key_of(r, r * kSelThreads + tid));
+    }
+  };
+  auto scan_excl = [&](uint32_t v, uint32_t& total) __attribute__((always_inline)) -> uint32_t {
+    uint32_t incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t t = __shfl_up(incl, o);
+      if (lane >= o) incl += t;
+    }
+    if (lane == kWave - 1) s_tot[wave] = incl;
+    __syncthreads();
+    uint32_t before = 0;
+    total = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+      const uint32_t t = s_tot[w];
+      before += w < wave ? t : 0u;
+      total += t;
+    }
+    __syncthreads();  // s_tot is rewritten by the next scan
+    return before + incl - v;
+  };
+  uint32_t base_eq = 0, base_sel = 0;
+  for (int r0 = 0; r0 < nr; r0 += CH) {
+    for_rounds(r0, [&](int r, uint32_t key) __attribute__((always_inline)) {
+      const int i = r * kSelThreads + tid;
       const bool valid = i < L;
-      const uint32_t key = key_of(rr, i);
+      const uint64_t bgt = __ballot(valid && key > thr);
+      const uint64_t beq = __ballot(valid && take_eq && key == thr);
+      if (lane == 0) {
+        c_eq[(r - r0) * kSelWaves + wave] = static_cast<uint32_t>(__popcll(beq));
+        c_sel[(r - r0) * kSelWaves + wave] = static_cast<uint32_t>(__popcll(bgt));
+      }
+    });
+    __syncthreads();
+    const bool ent = r0 + tid / kSelWaves < nr;  // this thread's pair exists
+    const uint32_t veq = ent ? c_eq[tid] : 0u, vgt = ent ? c_sel[tid] : 0u;
+    uint32_t tot_eq, tot_sel;
+    const uint32_t rank = base_eq + scan_excl(veq, tot_eq);
+    const uint32_t take = need_eq > rank ? (need_eq - rank < veq ? need_eq - rank : veq) : 0u;
+    const uint32_t first = base_sel + scan_excl(vgt + take, tot_sel);
+    c_eq[tid] = rank;
+    c_sel[tid] = first;
+    base_eq += tot_eq;
+    base_sel += tot_sel;
+    __syncthreads();
+    for_rounds(r0, [&](int r, uint32_t key) __attribute__((always_inline)) {
+      const int i = r * kSelThreads + tid;
+      const bool valid = i < L;
       const bool gt = valid && key > thr;
       const bool eq = valid && take_eq && key == thr;
       const uint64_t beq = __ballot(eq);
-      if (lane == 0) wcnt[0][wave] = static_cast<uint32_t>(__popcll(beq));
-      __syncthreads();
-      uint32_t eq_before = base_eq, eq_total = 0;
-      for (int w = 0; w < kSelWaves; ++w) {
-        const uint32_t v = wcnt[0][w];
-        if (w < wave) eq_before += v;
-        eq_total += v;
-      }
-      eq_before += static_cast<uint32_t>(__popcll(beq & lt_mask));
+      const uint32_t eq_before = c_eq[(r - r0) * kSelWaves + wave] + static_cast<uint32_t>(__popcll(beq & lt_mask));
       const bool sel = gt || (eq && eq_before < need_eq);
       const uint64_t bsel = __ballot(sel);
-      if (lane == 0) wcnt[1][wave] = static_cast<uint32_t>(__popcll(bsel));
-      __syncthreads();
-      uint32_t pos = base_sel, sel_total = 0;
-      for (int w = 0; w < kSelWaves; ++w) {
-        const uint32_t v = wcnt[1][w];
-        if (w < wave) pos += v;
-        sel_total += v;
-      }
-      pos += static_cast<uint32_t>(__popcll(bsel & lt_mask));
+      const uint32_t pos = c_sel[(r - r0) * kSelWaves + wave] + static_cast<uint32_t>(__popcll(bsel & lt_mask));
       if (valid) {
         mask[i] = sel ? 1 : 0;
         if (sel) idx[pos] = idx_base + i;
       }
-      base_eq += eq_total;
-      base_sel += sel_total;
-      __syncthreads();  // wcnt is rewritten by the next chunk
-    }
+    });
+    __syncthreads();  // c_eq / c_sel are rewritten by the next chunk
   }
   if (tid == 0 && n_sel != nullptr) *n_sel = static_cast<int32_t>(base_sel);
 }

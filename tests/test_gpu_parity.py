@@ -49,6 +49,20 @@ def test_energy_matches_oracle(profile, n, T):
         assert (ge[: T // 2] == 0).all()
 
 
+@pytest.mark.parametrize("n_fft,hop,bands", [(514, 160, 8), (256, 100, 6), (2048, 512, 16), (18, 7, 3)])
+def test_energy_other_stft_sizes(n_fft, hop, bands):
+    """Window lengths that are not a multiple of 4 (the DFT's four-way
+    unrolled sum then has a two-term tail), short and long windows."""
+    say(f"energy n_fft={n_fft} hop={hop} bands={bands}")
+    audio = synth.make_audio("speech", 20000, 16000, seed=12)
+    Eb, e, w = OE.energy(audio, 5, 16000, n_fft, hop, bands)
+    gb, ge, gw = api.energy(up(audio), 5, 16000, n_fft, hop, bands)
+    torch.cuda.synchronize()
+    for got, want, name in ((down(gb), Eb, "band"), (down(ge), e, "frame"), (down(gw), w, "weight")):
+        err = np.abs(got.astype(np.float64) - want)
+        assert (err <= 1e-6 * np.abs(want.astype(np.float64))).all(), (name, float(err.max()))
+
+
 # ------------------------------------------------------------------- select
 
 def _frame_weight(w, profile=None):
