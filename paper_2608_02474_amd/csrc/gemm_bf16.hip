@@ -83,26 +83,29 @@ __device__ __forceinline__ void gemm_col4(const GemmBf16Args& p, int col, float*
   }
 }
 
+// Residual of the 4 consecutive columns col .. col+3 of row `row` (gathered
+// through res_rows if given), bf16 or fp32, as fp32.
+__device__ __forceinline__ void gemm_res4(const GemmBf16Args& p, int row, int col, float* res) {
+  const int64_t rr = p.res_rows ? p.res_rows[row] : row;
+  if (p.res_bf16) {
+    const uint2 rb = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
+    res[0] = __uint_as_float(rb.x << 16);
+    res[1] = __uint_as_float(rb.x & 0xffff0000u);
+    res[2] = __uint_as_float(rb.y << 16);
+    res[3] = __uint_as_float(rb.y & 0xffff0000u);
+  } else {
+    const float4 rf = *reinterpret_cast<const float4*>(static_cast<const float*>(p.res) + rr * p.ldr + col);
+    res[0] = rf.x; res[1] = rf.y; res[2] = rf.z; res[3] = rf.w;
+  }
+}
+
 // Output of 4 consecutive columns col .. col+3 of row `row` (acc4 = sums
-// without bias): bias, then GELU (bf16 out), plain (bf16 out) or residual +
-// gate * v (fp32 out).
+// without bias; res = the residual of those columns for EPI_GATE_RES).
 template <int EPI>
 __device__ __forceinline__ void gemm_store4(const GemmBf16Args& p, int row, int col, const float* acc4,
-                                            const float* bias, const float* gate) {
+                                            const float* bias, const float* gate, const float* res) {
   float v[4] = {acc4[0] + bias[0], acc4[1] + bias[1], acc4[2] + bias[2], acc4[3] + bias[3]};
   if (EPI == EPI_GATE_RES) {
-    const int64_t rr = p.res_rows ? p.res_rows[row] : row;
-    float res[4];
-    if (p.res_bf16) {
-      const uint2 rb = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
-      res[0] = __uint_as_float(rb.x << 16);
-      res[1] = __uint_as_float(rb.x & 0xffff0000u);
-      res[2] = __uint_as_float(rb.y << 16);
-      res[3] = __uint_as_float(rb.y & 0xffff0000u);
-    } else {
-      const float4 rf = *reinterpret_cast<const float4*>(static_cast<const float*>(p.res) + rr * p.ldr + col);
-      res[0] = rf.x; res[1] = rf.y; res[2] = rf.z; res[3] = rf.w;
-    }
     float4 o;
     o.x = res[0] + gate[0] * v[0];
     o.y = res[1] + gate[1] * v[1];
@@ -342,16 +345,64 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
   const int col = n0 + wn * (BN / WN) + c_l;           // global column (4 | col)
   float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (!split_k) gemm_col4<EPI>(p, col, bias, gate);
+  constexpr int NQ = 32 / RPI;                     // row groups of a slab per lane
+  constexpr int NR = EPI == EPI_GATE_RES ? NQ : 1;
 #pragma unroll
   for (int i = 0; i < C::kTM; ++i) {
+    // the residuals of this lane's rows of the slab: every row index, then
+    // every residual, loaded together (rows past M load row M - 1, unused),
+    // in flight while the slab is staged
+    float res[NR][4];
+    if constexpr (EPI == EPI_GATE_RES) {
+      if (!split_k) {
+        int64_t rr[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+          const int row = m0 + wm * (BM / WM) + i * 32 + q * RPI + lane / LPR;
+          rr[q] = row < p.M ? row : p.M - 1;
+        }
+        if (p.res_rows != nullptr) {
+          int g[NQ];
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) g[q] = p.res_rows[rr[q]];
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) rr[q] = g[q];
+        }
+        if (p.res_bf16) {
+          const bf16_t* rb = static_cast<const bf16_t*>(p.res) + col;
+          uint2 raw[NQ];
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) raw[q] = *reinterpret_cast<const uint2*>(rb + rr[q] * p.ldr);
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) {
+            res[q][0] = __uint_as_float(raw[q].x << 16);
+            res[q][1] = __uint_as_float(raw[q].x & 0xffff0000u);
+            res[q][2] = __uint_as_float(raw[q].y << 16);
+            res[q][3] = __uint_as_float(raw[q].y & 0xffff0000u);
+          }
+        } else {
+          const float* rf = static_cast<const float*>(p.res) + col;
+          float4 raw[NQ];
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) raw[q] = *reinterpret_cast<const float4*>(rf + rr[q] * p.ldr);
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) {
+            res[q][0] = raw[q].x;
+            res[q][1] = raw[q].y;
+            res[q][2] = raw[q].z;
+            res[q][3] = raw[q].w;
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int j = 0; j < C::kTN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         ep[(8 * (r >> 2) + 4 * hi + (r & 3)) * EP_LD + j * 32 + l32] = acc[i][j][r];
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(63));  // this wave's staged slab is in LDS
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(63));  // this wave's staged slab is in LDS (LDS only)
 #pragma unroll
-    for (int q = 0; q < 32 / RPI; ++q) {
+    for (int q = 0; q < NQ; ++q) {
       const int r_l = q * RPI + lane / LPR;
       const int trow = wm * (BM / WM) + i * 32 + r_l;  // row within the tile
       const float4 a4 = *reinterpret_cast<const float4*>(ep + r_l * EP_LD + c_l);
@@ -361,7 +412,7 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
                                    static_cast<int64_t>(trow) * BN + (col - n0)) = a4;
       } else if (m0 + trow < p.M) {
         const float v[4] = {a4.x, a4.y, a4.z, a4.w};
-        gemm_store4<EPI>(p, m0 + trow, col, v, bias, gate);
+        gemm_store4<EPI>(p, m0 + trow, col, v, bias, gate, res[EPI == EPI_GATE_RES ? q : 0]);
       }
     }
   }
@@ -389,9 +440,10 @@ __global__ void __launch_bounds__(256) gemm_splitk_reduce(GemmBf16Args p, int nt
     v[2] += a4.z;
     v[3] += a4.w;
   }
-  float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f}, res[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   gemm_col4<EPI>(p, tile_n * BN + 4 * c4, bias, gate);
-  gemm_store4<EPI>(p, row, tile_n * BN + 4 * c4, v, bias, gate);
+  if (EPI == EPI_GATE_RES) gemm_res4(p, row, tile_n * BN + 4 * c4, res);
+  gemm_store4<EPI>(p, row, tile_n * BN + 4 * c4, v, bias, gate, res);
 }
 
 template <int BM, int BN, int WM, int WN, int NS, int BK, int EPI>
