@@ -26,6 +26,15 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return static_cast<bf16_t>(u >> 16);
 }
 
+// Two floats rounded to bf16 (nearest even) and packed, low half first, by
+// the hardware conversion (v_cvt_pk_bf16_f32): the same rounding as
+// f32_to_bf16 for every non-NaN value, in one instruction.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 // Element loads/stores that hide the storage type.
 template <typename T> struct Elem;
 template <> struct Elem<float> {
