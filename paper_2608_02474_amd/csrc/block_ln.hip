@@ -129,12 +129,121 @@ modln_rows(const Tin* __restrict__ x, int M, int D, const float* __restrict__ sh
   }
 }
 
+// The same LayerNorm with the modulation vectors staged once per workgroup in
+// LDS (1 + scale, then shift: 8 D bytes) and each wave looping over rows
+// (row = 4 * blockIdx.x + wave, then in steps of 4 * gridDim.x).  Reading the
+// two vectors from L2 for every row used to move four times the row's own
+// bytes through the load path; from LDS they cost two 16-byte reads per
+// eight elements.  Requires MAXC > 0 and D <= kLnLdsMaxD.
+constexpr int kLnLdsMaxD = 8192;
+
+template <typename Tin, typename Tout, int MAXC>
+__global__ void __launch_bounds__(kLnThreads)
+modln_rows_lds(const Tin* __restrict__ x, int M, int D, const float* __restrict__ shift,
+               const float* __restrict__ scale, float eps, Tout* __restrict__ out) {
+  extern __shared__ float4 lds_mod4[];
+  float* s1 = reinterpret_cast<float*>(lds_mod4);  // [D] 1 + scale
+  float* sh = s1 + D;                              // [D] shift
+  for (int i = threadIdx.x; i < D / 4; i += kLnThreads) {
+    float4 a = reinterpret_cast<const float4*>(scale)[i];
+    a.x += 1.0f;
+    a.y += 1.0f;
+    a.z += 1.0f;
+    a.w += 1.0f;
+    reinterpret_cast<float4*>(s1)[i] = a;
+    reinterpret_cast<float4*>(sh)[i] = reinterpret_cast<const float4*>(shift)[i];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int nch = D / 8;
+  const float invD = 1.0f / static_cast<float>(D);
+  constexpr int R = MAXC;
+  auto body = [&](auto full_c, const Tin* xr, Tout* orow) __attribute__((always_inline)) {
+    constexpr bool FULL = decltype(full_c)::value;  // every lane owns R chunks
+    Raw8<Tin> raw[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int c = lane + u * kWave;
+      raw[u].load(xr + (FULL || c < nch ? c : nch - 1) * 8);
+    }
+    float sum = 0.0f;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      float v[8];
+      raw[u].unpack(v);
+      const bool ok = FULL || lane + u * kWave < nch;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sum += ok ? v[j] : 0.0f;
+    }
+    const float mean = wave_sum(sum) * invD;
+    float sq = 0.0f;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      float v[8];
+      raw[u].unpack(v);
+      const bool ok = FULL || lane + u * kWave < nch;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float d = v[j] - mean;
+        sq += ok ? d * d : 0.0f;
+      }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(sq) * invD + eps);
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int c = lane + u * kWave;
+      if (FULL || c < nch) {
+        float v[8], o[8], sc[8], shv[8];
+        raw[u].unpack(v);
+        const float4* a = reinterpret_cast<const float4*>(s1 + c * 8);
+        const float4* b = reinterpret_cast<const float4*>(sh + c * 8);
+        const float4 a0 = a[0], a1 = a[1], b0 = b[0], b1 = b[1];
+        sc[0] = a0.x; sc[1] = a0.y; sc[2] = a0.z; sc[3] = a0.w;
+        sc[4] = a1.x; sc[5] = a1.y; sc[6] = a1.z; sc[7] = a1.w;
+        shv[0] = b0.x; shv[1] = b0.y; shv[2] = b0.z; shv[3] = b0.w;
+        shv[4] = b1.x; shv[5] = b1.y; shv[6] = b1.z; shv[7] = b1.w;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = (v[j] - mean) * rstd * sc[j] + shv[j];
+        ln_store8(orow + c * 8, o);
+      }
+    }
+  };
+  const int64_t step = static_cast<int64_t>(gridDim.x) * kLnWaves;
+  for (int64_t row = static_cast<int64_t>(blockIdx.x) * kLnWaves + wave; row < M; row += step) {
+    if (nch == R * kWave)
+      body(std::integral_constant<bool, true>{}, x + row * D, out + row * D);
+    else
+      body(std::integral_constant<bool, false>{}, x + row * D, out + row * D);
+  }
+}
+
 template <typename Tin, typename Tout>
 static hipError_t launch_modln_t(const char* name, const Tin* x, int M, int D, const float* shift,
                                  const float* scale, float eps, Tout* out, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
   const dim3 grid((M + kLnWaves - 1) / kLnWaves);
   const int per_lane = (D / 8 + kWave - 1) / kWave;
+  if (D <= kLnLdsMaxD) {
+    // four workgroups per CU (the LDS of the modulation vectors allows four
+    // at the largest D), each wave looping over its rows
+    const int cap = 4 * device_cu_count();
+    const dim3 grid_l(static_cast<unsigned>(grid.x < static_cast<unsigned>(cap) ? grid.x : cap));
+    const size_t lds = sizeof(float) * 2 * static_cast<size_t>(D);
+#define ECHO_LNL_CASE(MC)                                                                           \
+  if (per_lane <= MC)                                                                               \
+    return ECHO_LAUNCH(name, (modln_rows_lds<Tin, Tout, MC>), grid_l, dim3(kLnThreads), lds, stream, x, \
+                       M, D, shift, scale, eps, out);
+    ECHO_LNL_CASE(1)
+    ECHO_LNL_CASE(2)
+    ECHO_LNL_CASE(3)
+    ECHO_LNL_CASE(4)
+    ECHO_LNL_CASE(6)
+    ECHO_LNL_CASE(8)
+    ECHO_LNL_CASE(10)
+    ECHO_LNL_CASE(12)
+    ECHO_LNL_CASE(16)
+#undef ECHO_LNL_CASE
+  }
 #define ECHO_LN_CASE(MC)                                                                       \
   if (per_lane <= MC)                                                                          \
     return ECHO_LAUNCH(name, (modln_rows<Tin, Tout, MC>), grid, dim3(kLnThreads), 0, stream, x, \
