@@ -434,7 +434,10 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     s_half(smem + STN * ATT_TILE_BYTES, KBN, sn, [&](int i) __attribute__((always_inline)) {
       exp_chunk(sc, i, neg_mc, psum, pf);
       if constexpr (KBN == 0) {
-        if (i % 2 == 1 && i / 2 < 2 * NLD) tile_copy(i / 2);
+        // the wave's 2 NLD copies of the tile, spread evenly over the 8 MFMAs
+        constexpr int NC = 2 * NLD;
+#pragma unroll
+        for (int c = (i * NC) / 8; c < ((i + 1) * NC) / 8; ++c) tile_copy(c);
       }
     });
     exp_end(psum);
