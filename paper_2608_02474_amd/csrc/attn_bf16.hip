@@ -295,20 +295,21 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // O += V^T P^T for one half (8 MFMAs: dh block d = i / 2, 16-key half
-  // a = i % 2) with `work(i)` placed after MFMA i
+  // O += V^T P^T for one half (8 MFMAs: 16-key half a = i / 4, dh block
+  // d = i % 4, so that the first four use only the probabilities of keys
+  // 0-15) with `work(i)` placed after MFMA i
   auto pv_half = [&](const char* vs, int kb, const bf16x8(&pf)[QB][2], auto&& work) __attribute__((always_inline)) {
     bf16x8 ring[ATT_RING];
 #pragma unroll
-    for (int i = 0; i < ATT_RING; ++i) ring[i] = read_v(vs, kb, i / 2, i % 2);
+    for (int i = 0; i < ATT_RING; ++i) ring[i] = read_v(vs, kb, i % 4, i / 4);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int d = i / 2, a = i % 2;
+      const int d = i % 4, a = i / 4;
       const bf16x8 va = ring[i % ATT_RING];
 #pragma unroll
       for (int b = 0; b < QB; ++b)
         o[b][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[b][a], o[b][d], 0, 0, 0);
-      if (i + ATT_RING < 8) ring[i % ATT_RING] = read_v(vs, kb, (i + ATT_RING) / 2, (i + ATT_RING) % 2);
+      if (i + ATT_RING < 8) ring[i % ATT_RING] = read_v(vs, kb, (i + ATT_RING) % 4, (i + ATT_RING) / 4);
       work(i);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -358,6 +359,37 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       pf[b][a][j] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sh[b][8 * a + j], scale_log2, neg_mc[b])));
       pf[b][a][j + 1] =
           static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sh[b][8 * a + j + 1], scale_log2, neg_mc[b])));
+      const bf16x2 pair = {pf[b][a][j], pf[b][a][j + 1]};
+      psum[b] = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, psum[b], false);
+    }
+  };
+  // The same three steps split for software pipelining across chunks, so
+  // that the vector work placed after one MFMA has no dependence inside it:
+  // the scaled, shifted scores of chunk c; their exp2; the bf16 pack and row
+  // sum (same operations and order as exp_chunk).
+  auto exp_arg = [&](const f32x16(&sh)[QB], int c, const float(&neg_mc)[QB], float(&t)[QB][2])
+      __attribute__((always_inline)) {
+    const int a = c / 4, j = 2 * (c % 4);
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      t[b][0] = fmaf(sh[b][8 * a + j], scale_log2, neg_mc[b]);
+      t[b][1] = fmaf(sh[b][8 * a + j + 1], scale_log2, neg_mc[b]);
+    }
+  };
+  auto exp_val = [&](float(&t)[QB][2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      t[b][0] = __builtin_amdgcn_exp2f(t[b][0]);
+      t[b][1] = __builtin_amdgcn_exp2f(t[b][1]);
+    }
+  };
+  auto exp_pack = [&](int c, const float(&t)[QB][2], float(&psum)[QB], bf16x8(&pf)[QB][2])
+      __attribute__((always_inline)) {
+    const int a = c / 4, j = 2 * (c % 4);
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      pf[b][a][j] = static_cast<__bf16>(t[b][0]);
+      pf[b][a][j + 1] = static_cast<__bf16>(t[b][1]);
       const bf16x2 pair = {pf[b][a][j], pf[b][a][j + 1]};
       psum[b] = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, psum[b], false);
     }
@@ -431,8 +463,14 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       __syncthreads();
       tile_prep((h + 1) / 2 + 2, (STN + 2) % ATT_NSTAGE);
     }
+    // chunk c: arguments after S MFMA c, exp2 after MFMA c + 1, pack and
+    // row sum after MFMA c + 2; chunk 7's exp2 and the packs of chunks 6
+    // and 7 go under the first PV MFMAs (which read keys 0-15 only)
+    float tq[3][QB][2];
     s_half(smem + STN * ATT_TILE_BYTES, KBN, sn, [&](int i) __attribute__((always_inline)) {
-      exp_chunk(sc, i, neg_mc, psum, pf);
+      exp_arg(sc, i, neg_mc, tq[i % 3]);
+      if (i >= 1) exp_val(tq[(i + 2) % 3]);
+      if (i >= 2) exp_pack(i - 2, tq[(i + 1) % 3], psum, pf);
       if constexpr (KBN == 0) {
         // the wave's 2 NLD copies of the tile, spread evenly over the 8 MFMAs
         constexpr int NC = 2 * NLD;
@@ -440,10 +478,16 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
         for (int c = (i * NC) / 8; c < ((i + 1) * NC) / 8; ++c) tile_copy(c);
       }
     });
-    exp_end(psum);
     fresh_max(m);
-    pv_half(smem + ST * ATT_TILE_BYTES, KB, pf,
-            [&](int i) __attribute__((always_inline)) { max_chunk(sn, i, m); });
+    pv_half(smem + ST * ATT_TILE_BYTES, KB, pf, [&](int i) __attribute__((always_inline)) {
+      if (i == 0) {
+        exp_val(tq[7 % 3]);
+        exp_pack(6, tq[6 % 3], psum, pf);
+      }
+      if (i == 1) exp_pack(7, tq[7 % 3], psum, pf);
+      max_chunk(sn, i, m);
+    });
+    exp_end(psum);
     update_max(m);
   };
   int h = 0;
