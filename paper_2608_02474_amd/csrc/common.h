@@ -65,10 +65,10 @@ __device__ __forceinline__ void unpack16(const uint4& v, float* out, const float
 }
 __device__ __forceinline__ uint4 pack16(const float* in, const bf16_t*) {
   uint4 v;
-  v.x = f32_to_bf16(in[0]) | (static_cast<uint32_t>(f32_to_bf16(in[1])) << 16);
-  v.y = f32_to_bf16(in[2]) | (static_cast<uint32_t>(f32_to_bf16(in[3])) << 16);
-  v.z = f32_to_bf16(in[4]) | (static_cast<uint32_t>(f32_to_bf16(in[5])) << 16);
-  v.w = f32_to_bf16(in[6]) | (static_cast<uint32_t>(f32_to_bf16(in[7])) << 16);
+  v.x = pack_bf16x2(in[0], in[1]);
+  v.y = pack_bf16x2(in[2], in[3]);
+  v.z = pack_bf16x2(in[4], in[5]);
+  v.w = pack_bf16x2(in[6], in[7]);
   return v;
 }
 __device__ __forceinline__ uint4 pack16(const float* in, const float*) {
