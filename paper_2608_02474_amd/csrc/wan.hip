@@ -94,13 +94,13 @@ qk_norm_rope_rows(bf16_t* __restrict__ z, int64_t ldz, int M, int D, const float
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int jp = p0 + q;
-      float2 cs;
-      if (jp < geo.nt)
-        cs = tab_t[t * geo.nt + jp];
-      else if (jp < geo.nt + geo.nr)
-        cs = tab_r[r * geo.nr + (jp - geo.nt)];
-      else
-        cs = tab_c[c * geo.nc + (jp - geo.nt - geo.nr)];
+      // table entry of the pair's axis, chosen without a branch (lanes of a
+      // wave hold pairs of different axes)
+      const int it = t * geo.nt + jp;
+      const int ir = (tab_r - tab_t) + r * geo.nr + (jp - geo.nt);
+      const int ic = (tab_c - tab_t) + c * geo.nc + (jp - geo.nt - geo.nr);
+      const int e = jp < geo.nt ? it : (jp < geo.nt + geo.nr ? ir : ic);
+      const float2 cs = tab_t[e];
       const float a = v[2 * q], b = v[2 * q + 1];
       v[2 * q] = __fsub_rn(__fmul_rn(a, cs.x), __fmul_rn(b, cs.y));
       v[2 * q + 1] = __fadd_rn(__fmul_rn(a, cs.y), __fmul_rn(b, cs.x));
