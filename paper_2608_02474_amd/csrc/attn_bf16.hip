@@ -578,27 +578,29 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
 
 // Merge the key-range splits of the tail items: o = sum_s 2^{(m_s - m) c} o_s
 // / sum_s 2^{(m_s - m) c} l_s with m = max_s m_s (c = scale * log2 e).  One
-// thread per (item, query, dh) output element, splits added in order.
+// thread per output element, taken in the order the partials are stored (the
+// accumulator layout: lane fastest), so that every split's partial is read
+// with consecutive addresses; splits added in order.
 template <int QB, int WAVES>
 __global__ void __launch_bounds__(256)
 attn_combine(const float* __restrict__ part_o, const float* __restrict__ part_ml, int nitems,
              int nsplit, int item_base, int Mq, int H, float scale_log2, bf16_t* __restrict__ out,
              int64_t ldo) {
   typedef AttCfg<QB, WAVES> C;
+  constexpr int64_t kUnit = static_cast<int64_t>(C::kQ) * ATT_DH;  // partial floats per unit
   const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (e >= static_cast<int64_t>(nitems) * C::kQ * ATT_DH) return;
-  const int dh = static_cast<int>(e % ATT_DH);
-  const int qloc = static_cast<int>((e / ATT_DH) % C::kQ);
-  const int j = static_cast<int>(e / (static_cast<int64_t>(ATT_DH) * C::kQ));
+  if (e >= static_cast<int64_t>(nitems) * kUnit) return;
+  const int j = static_cast<int>(e / kUnit);
+  const int o = static_cast<int>(e % kUnit);
+  // storage order within a unit: ((wave * QB + b) * 64 + d * 16 + r) * 64 + lane
+  const int lane = o % kWave, dr = (o / kWave) % 64, wb = o / (kWave * 64);
+  const int d = dr / 16, r = dr % 16, l32 = lane & 31, hi = lane >> 5;
+  const int qloc = wb * 32 + l32;  // (wave * QB + b) * 32 + l32
+  const int dh = d * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
   const int ntq = (Mq + C::kQ - 1) / C::kQ;
   const int item = item_base + j, head = item / ntq, qt = item % ntq;
   const int qg = qt * C::kQ + qloc;
   if (qg >= Mq) return;
-  // accumulator coordinates of (qloc, dh)
-  const int wave = qloc / (QB * 32), b = (qloc / 32) % QB, l32 = qloc % 32;
-  const int d = dh / 32, rem = dh % 32;
-  const int hi = (rem >> 2) & 1, r = 4 * (rem >> 3) + (rem & 3);
-  const int lane = l32 + 32 * hi;
   float m = -INFINITY;
   for (int sp = 0; sp < nsplit; ++sp) {
     const int64_t unit = static_cast<int64_t>(j) * nsplit + sp;
@@ -609,7 +611,7 @@ attn_combine(const float* __restrict__ part_o, const float* __restrict__ part_ml
     const int64_t unit = static_cast<int64_t>(j) * nsplit + sp;
     const float w = __builtin_amdgcn_exp2f((part_ml[(unit * C::kQ + qloc) * 2] - m) * scale_log2);
     lsum += w * part_ml[(unit * C::kQ + qloc) * 2 + 1];
-    acc += w * part_o[((unit * WAVES + wave) * QB + b) * (4 * 16 * kWave) + (d * 16 + r) * kWave + lane];
+    acc += w * part_o[unit * kUnit + o];
   }
   out[static_cast<int64_t>(qg) * ldo + static_cast<int64_t>(head) * ATT_DH + dh] = f32_to_bf16(acc / lsum);
 }
