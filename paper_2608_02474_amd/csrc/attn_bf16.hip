@@ -4,7 +4,10 @@
 // with fp32 accumulation and an online (streaming) softmax.
 //
 // gfx950 mapping.  A workgroup of WAVES waves owns WAVES * QB * 32 queries of
-// one head (each wave QB blocks of 32 queries).  Keys stream in tiles of 64:
+// one head (each wave QB blocks of 32 queries).  The build uses 12 waves of
+// 32 queries: three waves per SIMD (168 registers each), and each K/V tile
+// copied to LDS serves 384 queries (a third fewer copies and barriers per
+// query than 8 waves).  Keys stream in tiles of 64:
 //   * K and V tiles are copied HBM/L2 -> LDS by direct global-to-LDS loads
 //     (global_load_lds_dwordx4: no VGPR staging), row-major [key][dh], into a
 //     4-stage ring.  Each lane fetches the 16-byte piece whose swizzled LDS
@@ -64,8 +67,11 @@ template <int QB, int WAVES>
 struct AttCfg {
   static constexpr int kThreads = WAVES * 64;
   static constexpr int kQ = WAVES * QB * 32;  // queries per workgroup
-  static constexpr int kLdsBytes = (2 * ATT_V_BASE > kQ * ATT_OS_STRIDE * 2)
-                                       ? 2 * ATT_V_BASE
+  // ring, then (when WAVES does not divide 16) 1 KB per wave with no third piece
+  static constexpr int kJunk = 16 % WAVES == 0 ? 0 : 1024 * (WAVES - 16 % WAVES);
+  static constexpr int kRingBytes = 2 * ATT_V_BASE + kJunk;
+  static constexpr int kLdsBytes = (kRingBytes > kQ * ATT_OS_STRIDE * 2)
+                                       ? kRingBytes
                                        : kQ * ATT_OS_STRIDE * 2;
 };
 
@@ -111,8 +117,17 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
               bf16_t* __restrict__ out, int64_t ldo, int item_base, int nsplit, int kt_per_split,
               float* __restrict__ part_o, float* __restrict__ part_ml) {
   typedef AttCfg<QB, WAVES> C;
-  constexpr int NLD = 16 / WAVES;  // 1 KB direct-load instructions per wave per K (or V) tile
-  static_assert(16 % WAVES == 0, "16 KB tiles split evenly over the waves");
+  // Direct-load plan: a K (or V) tile is 16 pieces of 1 KB (piece m = tile
+  // rows 4m .. 4m+3).  When WAVES divides 16, wave w copies the K and V
+  // pieces w + WAVES n.  Otherwise (12 waves) every wave copies three pieces:
+  // K piece w, V piece w, and a third one: K piece 12 + w for waves 0-3,
+  // V piece 12 + (w - 4) for waves 4-7, and for waves 8-11 a re-copy of its
+  // K row into a private 1 KB LDS area nobody reads, so that every wave has
+  // the same copy count and no branch (4 KB more per 32 KB tile).
+  constexpr bool EVEN = 16 % WAVES == 0;
+  constexpr int NLD = EVEN ? 16 / WAVES : 1;  // K (and V) pieces per wave in the regular slots
+  constexpr int NC = EVEN ? 2 * NLD : 3;      // copies per wave per tile
+  static_assert(EVEN || (WAVES == 12 && 16 - WAVES == 4), "12 waves: 4 extra K and 4 extra V pieces");
   __shared__ __attribute__((aligned(1024))) char smem[C::kLdsBytes];
 
   const int tid = threadIdx.x;
@@ -157,50 +172,42 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   // counter also holds the copies of the next two tiles.
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
-  // ---- direct-load plan: instruction n of this wave fills tile rows 4m .. 4m+3
-  // (m = wave + WAVES n); the lane lands in row 4m + lane/16, slot lane%16.
-  uint32_t row_off[NLD];             // byte offset of the lane's row within a tile
-  uint32_t k_src[NLD], v_src[NLD];   // byte offsets within a row
+  // ---- direct-load plan: regular slot n of this wave holds K and V piece
+  // m = wave + WAVES n; the lane lands in row 4m + lane/16, slot lane%16.
+  // Bits 0-3 of the row, and with them the swizzled slots, are the same for
+  // every piece of a wave (WAVES is a multiple of 4).
+  static_assert(WAVES % 4 == 0, "row bits 0-3 shared by a wave's pieces");
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t ldkv2 = static_cast<uint32_t>(ldkv) * 2u;
+  uint32_t row_off[NLD];  // byte offset of the lane's row within a tile
 #pragma unroll
-  for (int n = 0; n < NLD; ++n) {
-    const int r = 4 * (wave + WAVES * n) + g16;
-    const int p = i16;
-    const int ck = k_slot(r, p);                      // the XOR is its own inverse
-    const int cv = 2 * v_block(r, p >> 1) + (p & 1);
-    row_off[n] = static_cast<uint32_t>(r) * static_cast<uint32_t>(ldkv) * 2u;
-    k_src[n] = static_cast<uint32_t>(ck * 16);
-    v_src[n] = static_cast<uint32_t>(cv * 16);
-  }
+  for (int n = 0; n < NLD; ++n) row_off[n] = static_cast<uint32_t>(4 * (wave_u + WAVES * n) + g16) * ldkv2;
+  const int r0 = 4 * wave_u + g16;
+  const uint32_t k_src = static_cast<uint32_t>(k_slot(r0, i16) * 16);  // the XOR is its own inverse
+  const uint32_t v_src = static_cast<uint32_t>((2 * v_block(r0, i16 >> 1) + (i16 & 1)) * 16);
+  // third piece (uneven plans): K piece 12 + w (w < 4), V piece 8 + w
+  // (4 <= w < 8), else the private area; x_off is the piece's destination
+  // within a stage, or the area's absolute LDS offset
+  const bool x_v = !EVEN && wave_u >= 4 && wave_u < 8;
+  const bool x_junk = !EVEN && wave_u >= 8;
+  const int x_piece = wave_u < 4 ? 12 + wave_u : 8 + wave_u;
+  const uint32_t x_row = x_junk ? row_off[0] : static_cast<uint32_t>(4 * x_piece + g16) * ldkv2;
+  const uint32_t x_src = x_v ? v_src : k_src;
+  const uint32_t lds0 = lds_offset(smem);
+  const uint32_t x_off = x_junk ? lds0 + 2 * ATT_V_BASE + (wave_u - 8) * 1024
+                                : (x_v ? ATT_V_BASE : 0) + x_piece * 1024;
   const bf16_t* kh = k + hoff;
   const bf16_t* vh = v + hoff;
-  const uint32_t lds0 = lds_offset(smem);
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  // Copies of relative tile t into a stage.  Branch-free: the tile start is
-  // part of the uniform base and each lane clamps its row offset to the row
-  // L - 1 (rows past L are finite copies of row L - 1, masked later); a tile
-  // index past the last tile re-copies the last tile (into a stage that is
-  // free), so every wave always has the copies of exactly two tiles in flight
-  // after an issue and one wait count fits every iteration.
-  const uint32_t ldkv2 = static_cast<uint32_t>(ldkv) * 2u;
-  auto issue_tile = [&](int t, int stage) __attribute__((always_inline)) {
-    t = t < nkt ? t : nkt - 1;
-    const int key0 = (t_begin + t) * ATT_KT;
-    const bf16_t* kt = kh + static_cast<int64_t>(key0) * ldkv;
-    const bf16_t* vt = vh + static_cast<int64_t>(key0) * ldkv;
-    const uint32_t last = static_cast<uint32_t>(L - 1 - key0) * ldkv2;  // offset of row L - 1
-    const uint32_t kdst = lds0 + stage * ATT_TILE_BYTES;
-    const uint32_t vdst = kdst + ATT_V_BASE;
-#pragma unroll
-    for (int n = 0; n < NLD; ++n) {
-      const uint32_t m = static_cast<uint32_t>(wave_u + WAVES * n);
-      const uint32_t ro = row_off[n] < last ? row_off[n] : last;
-      lds_copy16_s(kt, ro + k_src[n], kdst + m * 1024);
-      lds_copy16_s(vt, ro + v_src[n], vdst + m * 1024);
-    }
-  };
 
-  // The same copies, issued one at a time: tile_prep() takes the tile's
-  // sources and stage; tile_copy(c) issues copy c (K then V of piece c / 2).
+  // Copies of relative tile t into a stage, issued one at a time:
+  // tile_prep() takes the tile's sources and stage; tile_copy(c) issues copy
+  // c (K then V of regular piece c / 2; the third piece last).  Branch-free:
+  // the tile start is part of the uniform base and each lane clamps its row
+  // offset to the row L - 1 (rows past L are finite copies of row L - 1,
+  // masked later); a tile index past the last tile re-copies the last tile
+  // (into a stage that is free), so every wave always has the copies of
+  // exactly two tiles in flight after an issue and one wait count fits every
+  // iteration.
   const bf16_t* pk_src = kh;
   const bf16_t* pv_src = vh;
   uint32_t p_last = 0, p_kdst = 0;
@@ -209,17 +216,27 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     const int key0 = (t_begin + t) * ATT_KT;
     pk_src = kh + static_cast<int64_t>(key0) * ldkv;
     pv_src = vh + static_cast<int64_t>(key0) * ldkv;
-    p_last = static_cast<uint32_t>(L - 1 - key0) * ldkv2;
+    p_last = static_cast<uint32_t>(L - 1 - key0) * ldkv2;  // offset of row L - 1
     p_kdst = lds0 + stage * ATT_TILE_BYTES;
   };
   auto tile_copy = [&](int c) __attribute__((always_inline)) {
+    if (!EVEN && c == 2) {
+      const uint32_t ro = x_row < p_last ? x_row : p_last;
+      lds_copy16_s(x_v ? pv_src : pk_src, ro + x_src, x_junk ? x_off : p_kdst + x_off);
+      return;
+    }
     const int n = c / 2;
     const uint32_t m = static_cast<uint32_t>(wave_u + WAVES * n);
     const uint32_t ro = row_off[n] < p_last ? row_off[n] : p_last;
     if (c % 2 == 0)
-      lds_copy16_s(pk_src, ro + k_src[n], p_kdst + m * 1024);
+      lds_copy16_s(pk_src, ro + k_src, p_kdst + m * 1024);
     else
-      lds_copy16_s(pv_src, ro + v_src[n], p_kdst + ATT_V_BASE + m * 1024);
+      lds_copy16_s(pv_src, ro + v_src, p_kdst + ATT_V_BASE + m * 1024);
+  };
+  auto issue_tile = [&](int t, int stage) __attribute__((always_inline)) {
+    tile_prep(t, stage);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) tile_copy(c);
   };
 
   // ---- precomputed LDS read addresses (byte offsets inside a stage)
@@ -233,15 +250,15 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   // V^T operand for dh block d, 16-key step (kb, a), half t: the lane (as a
   // source of the transpose read) addresses row kb*32 + 16a + 8(g16/2) + 4t +
   // i16/4 at dh d*32 + 16(g16%2) + 4(i16%4); it receives V[4 consecutive keys][its dh].
-  int v_rd[4][2];
+  // (half t adds 4 rows: the swizzle depends on row bits 0-1 only, so the
+  // second address is the first + 1024, an immediate offset)
+  int v_rd[4];
 #pragma unroll
-  for (int d = 0; d < 4; ++d)
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int rlow = 8 * (g16 >> 1) + 4 * t + (i16 >> 2);  // row within the 16-key step
-      const int blk = v_block(rlow, 2 * d + (g16 & 1));
-      v_rd[d][t] = ATT_V_BASE + rlow * 256 + blk * 32 + 8 * (i16 & 3);
-    }
+  for (int d = 0; d < 4; ++d) {
+    const int rlow = 8 * (g16 >> 1) + (i16 >> 2);  // row within the 16-key step (half 0)
+    const int blk = v_block(rlow, 2 * d + (g16 & 1));
+    v_rd[d] = ATT_V_BASE + rlow * 256 + blk * 32 + 8 * (i16 & 3);
+  }
 
   f32x16 o[QB][4];
 #pragma unroll
@@ -271,8 +288,8 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   // V^T fragment of PV step (d, a) for key block kb: dh block d, 16-key half a
   auto read_v = [&](const char* vs, int kb, int d, int a) __attribute__((always_inline)) {
     const int step = (kb * 32 + 16 * a) * 256;
-    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][0]));
-    const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d][1]));
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d]));
+    const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16(ECHO_LDS_V4(vs + step + v_rd[d] + 4 * 256));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
   };
   // Fragments flow through a ring of ATT_RING registers: the read for step
@@ -424,7 +441,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   const int nh_full = (L - key_begin) / 32 < nh ? (L - key_begin) / 32 : nh;  // halves with no key past L
   auto boundary = [&](int t, int stage_next2) __attribute__((always_inline)) {
     // this wave's copies of tile t have landed; those of tile t + 1 may be in flight
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(NC));
     __syncthreads();
     issue_tile(t + 2, stage_next2);
   };
@@ -459,7 +476,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     if constexpr (KBN == 0) {
       // this wave's copies of the new tile have landed; after the barrier
       // every wave is past the tile whose stage the copies below refill
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NLD * 2));
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NC));
       __syncthreads();
       tile_prep((h + 1) / 2 + 2, (STN + 2) % ATT_NSTAGE);
     }
@@ -472,8 +489,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       if (i >= 1) exp_val(tq[(i + 2) % 3]);
       if (i >= 2) exp_pack(i - 2, tq[(i + 1) % 3], psum, pf);
       if constexpr (KBN == 0) {
-        // the wave's 2 NLD copies of the tile, spread evenly over the 8 MFMAs
-        constexpr int NC = 2 * NLD;
+        // the wave's NC copies of the tile, spread evenly over the 8 MFMAs
 #pragma unroll
         for (int c = (i * NC) / 8; c < ((i + 1) * NC) / 8; ++c) tile_copy(c);
       }
@@ -667,13 +683,13 @@ hipError_t launch_attn_variant(const bf16_t* q, int64_t ldq, const bf16_t* k, co
 size_t attn_partial_bytes() {
   // 256 units (one per CU of a 256-CU device) of 256 queries x (128 outputs +
   // maximum + sum) floats; on a larger device the tail is split less
-  return sizeof(float) * 256 * 256 * (ATT_DH + 2);
+  return sizeof(float) * 256 * AttCfg<1, 12>::kQ * (ATT_DH + 2);
 }
 
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
                             float* part, size_t part_bytes, hipStream_t stream, const char* timing_name) {
-  return launch_attn_variant<1, 8>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, part, part_bytes, stream,
+  return launch_attn_variant<1, 12>(q, ldq, k, v, ldkv, Mq, L, H, out, ldo, part, part_bytes, stream,
                                    timing_name);
 }
 
