@@ -54,7 +54,7 @@ modln_rows(const Tin* __restrict__ x, int M, int D, const float* __restrict__ sh
 #pragma unroll
       for (int u = 0; u < R; ++u) {
         const int c = lane + u * kWave;
-        raw[u].load(xr + (FULL || c < nch ? c : nch - 1) * 8);
+        raw[u].load_nt(xr + (FULL || c < nch ? c : nch - 1) * 8);
       }
       float sum = 0.0f;
 #pragma unroll
@@ -164,7 +164,7 @@ modln_rows_lds(const Tin* __restrict__ x, int M, int D, const float* __restrict_
 #pragma unroll
     for (int u = 0; u < R; ++u) {
       const int c = lane + u * kWave;
-      raw[u].load(xr + (FULL || c < nch ? c : nch - 1) * 8);
+      raw[u].load_nt(xr + (FULL || c < nch ? c : nch - 1) * 8);
     }
     float sum = 0.0f;
 #pragma unroll

@@ -43,17 +43,17 @@ __device__ __forceinline__ void load8(const bf16_t* p, float* v) {
   unpack16(ldg16(p), v, static_cast<const bf16_t*>(nullptr));
 }
 __device__ __forceinline__ void store8(float* p, const float* v) {
-  stg16(p, pack16(v, static_cast<const float*>(nullptr)));
-  stg16(p + 4, pack16(v + 4, static_cast<const float*>(nullptr)));
+  stg16_nt(p, pack16(v, static_cast<const float*>(nullptr)));
+  stg16_nt(p + 4, pack16(v + 4, static_cast<const float*>(nullptr)));
 }
 __device__ __forceinline__ void store8(bf16_t* p, const float* v) {
-  stg16(p, pack16(v, static_cast<const bf16_t*>(nullptr)));
+  stg16_nt(p, pack16(v, static_cast<const bf16_t*>(nullptr)));
 }
 __device__ __forceinline__ void copy8(const float* src, float* dst) {
-  stg16(dst, ldg16(src));
-  stg16(dst + 4, ldg16(src + 4));
+  stg16_nt(dst, ldg16(src));
+  stg16_nt(dst + 4, ldg16(src + 4));
 }
-__device__ __forceinline__ void copy8(const bf16_t* src, bf16_t* dst) { stg16(dst, ldg16(src)); }
+__device__ __forceinline__ void copy8(const bf16_t* src, bf16_t* dst) { stg16_nt(dst, ldg16(src)); }
 
 // fp32(fp32(a * b) + c): multiply and add rounded separately, never fused.
 __device__ __forceinline__ float mul_add_unfused(float a, float b, float c) {
@@ -71,7 +71,7 @@ __device__ __forceinline__ void quantize8(const float* res, float inv, int8_t* d
     const uint32_t b = static_cast<uint32_t>(static_cast<int32_t>(q)) & 0xffu;
     w[j / 4] |= b << (8 * (j % 4));
   }
-  *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+  stg8_nt(dst, make_uint2(w[0], w[1]));
 }
 
 // MAXC > 0: the fresh row's residual stays in registers (D <= 512 * MAXC);
@@ -106,8 +106,8 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
         for (int u = 0; u < R; ++u) {
           const int c = lane + u * kWave;
           const int cc = FULL || c < nch ? c : nch - 1;
-          yraw[u].load(ys + cc * 8);
-          xraw[u].load(xi + cc * 8);
+          yraw[u].load_nt(ys + cc * 8);
+          xraw[u].load_nt(xi + cc * 8);
         }
 #pragma unroll
         for (int u = 0; u < R; ++u) {
@@ -117,7 +117,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
             yraw[u].unpack(yv);
             xraw[u].unpack(xv);
             store8(y + i * D + c * 8, yv);      // fresh output, cast to storage type
-            xraw[u].store(xref + i * D + c * 8);  // reference := current input
+            xraw[u].store_nt(xref + i * D + c * 8);  // reference := current input
             if constexpr (CODEC == kFull) {
               store8(store + i * D + c * 8, yv);
             } else {
@@ -194,7 +194,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
 #pragma unroll
       for (int u = 0; u < R; ++u) {
         const int c = lane + u * kWave;
-        if (c < nch) rr[u].store(y + i * D + c * 8);
+        if (c < nch) rr[u].store_nt(y + i * D + c * 8);
       }
     } else {
       for (int c = lane; c < nch; c += kWave) copy8(store + i * D + c * 8, y + i * D + c * 8);
@@ -224,8 +224,8 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
       for (int u = 0; u < R; ++u) {
         const int c = lane + u * kWave;
         const int cc = FULL || c < nch ? c : nch - 1;
-        if constexpr (CODEC != kNaiveInt8) rr[u].load(xref + i * D + cc * 8);
-        cw[u] = *reinterpret_cast<const uint2*>(codes + i * D + cc * 8);
+        if constexpr (CODEC != kNaiveInt8) rr[u].load_nt(xref + i * D + cc * 8);
+        cw[u] = ldg8_nt(codes + i * D + cc * 8);
       }
 #pragma unroll
       for (int u = 0; u < R; ++u) {

@@ -62,8 +62,8 @@ saliency_rows(const T* __restrict__ x, const T* __restrict__ xref, const float* 
     for (int u = 0; u < R; ++u) {
       const int c = lane + u * kWave;
       const int cc = c < nch ? c : nch - 1;  // past the row end: in-bounds re-load, not added
-      ra[u].load(xr + cc * 8);
-      rb[u].load(rr + cc * 8);
+      ra[u].load_nt(xr + cc * 8);
+      rb[u].load_nt(rr + cc * 8);
     }
 #pragma unroll
     for (int u = 0; u < R; ++u)
