@@ -95,6 +95,9 @@ step_delta_sum(const double* __restrict__ num, const double* __restrict__ den, i
   __shared__ double red_n[kSelWaves], red_d[kSelWaves];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   double a = 0.0, b = 0.0;
+  // unrolled so that eight loads of each array are in flight; the additions
+  // keep their order
+#pragma unroll 8
   for (int i = tid; i < L; i += kSelThreads) {
     a += num[i];
     b += den[i];

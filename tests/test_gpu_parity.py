@@ -234,6 +234,28 @@ def test_block_partial_full_compare(w):
         check_block(got, want, w.dtype, f"{w.name}/{name}")
 
 
+# bf16 shapes at the edges of the attention tiling: one ragged key tile, exactly
+# one tile, one tile plus one key, three tiles, and query sets that cross a
+# 384-query workgroup (with the key-split tail of a few items)
+EDGE = [synth.Workload(f"edge_bf16_{T * gh * gw}tok", T=T, grid=(gh, gw), D=256, H=2, F=512,
+                       n_samples=4000, ratio=0.5, dtype="bf16", audio="bursts", seed=30 + T * gh * gw)
+        for T, gh, gw in [(2, 4, 5), (1, 8, 8), (5, 1, 13), (2, 5, 13), (4, 10, 12)]]
+
+
+@pytest.mark.parametrize("w", EDGE, ids=lambda w: w.name)
+def test_block_partial_attention_edges(w):
+    p = synth.make_block_weights(w)
+    _, x = synth.make_latents(w)
+    rng = np.random.default_rng(11)
+    kv = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    for name, idx in {"half": np.sort(rng.choice(w.L, w.L // 2, replace=False)),
+                      "one": np.array([0]), "all": np.arange(w.L)}.items():
+        say(f"block {w.name} {name} n={len(idx)}")
+        got = _block_gpu(w, p, x, idx)
+        want = OB.block_partial(p, x, idx, w.H, kv=kv)
+        check_block(got, want, w.dtype, f"{w.name}/{name}")
+
+
 def test_block_gates_one_informational():
     # gates ~ N(1, 0.1): larger bf16 error budget; reported, bounded loosely
     w = RAGGED
