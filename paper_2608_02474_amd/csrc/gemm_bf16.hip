@@ -90,19 +90,23 @@ __device__ __forceinline__ void gemm_col4(const GemmBf16Args& p, int col, float*
 __device__ __forceinline__ void gemm_res4(const GemmBf16Args& p, int row, int col, float* res) {
   const int64_t rr = p.res_rows ? p.res_rows[row] : row;
   if (p.res_bf16) {
-    const uint2 rb = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
+    const uint2 rb = ldg8_nt(static_cast<const bf16_t*>(p.res) + rr * p.ldr + col);
     res[0] = __uint_as_float(rb.x << 16);
     res[1] = __uint_as_float(rb.x & 0xffff0000u);
     res[2] = __uint_as_float(rb.y << 16);
     res[3] = __uint_as_float(rb.y & 0xffff0000u);
   } else {
-    const float4 rf = *reinterpret_cast<const float4*>(static_cast<const float*>(p.res) + rr * p.ldr + col);
-    res[0] = rf.x; res[1] = rf.y; res[2] = rf.z; res[3] = rf.w;
+    const uint4 rf = ldg16_nt(static_cast<const float*>(p.res) + rr * p.ldr + col);
+    res[0] = __uint_as_float(rf.x); res[1] = __uint_as_float(rf.y); res[2] = __uint_as_float(rf.z); res[3] = __uint_as_float(rf.w);
   }
 }
 
 // Output of 4 consecutive columns col .. col+3 of row `row` (acc4 = sums
-// without bias; res = the residual of those columns for EPI_GATE_RES).
+// without bias; res = the residual of those columns for EPI_GATE_RES).  The
+// fp32 gate + residual outputs and their residual reads are streams read or
+// written once, so they use the non-temporal accesses (O projection
+// 0.687 -> 0.653 ms, FFN down 1.657 -> 1.645 ms); the bf16 outputs are read
+// by the next kernel and keep ordinary stores.
 template <int EPI>
 __device__ __forceinline__ void gemm_store4(const GemmBf16Args& p, int row, int col, const float* acc4,
                                             const float* bias, const float* gate, const float* res) {
@@ -113,7 +117,7 @@ __device__ __forceinline__ void gemm_store4(const GemmBf16Args& p, int row, int 
     o.y = res[1] + gate[1] * v[1];
     o.z = res[2] + gate[2] * v[2];
     o.w = res[3] + gate[3] * v[3];
-    *reinterpret_cast<float4*>(static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc + col) = o;
+    stg16_nt(static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc + col, make_uint4(__float_as_uint(o.x), __float_as_uint(o.y), __float_as_uint(o.z), __float_as_uint(o.w)));
   } else {
     if (EPI == EPI_GELU) {
 #pragma unroll
@@ -374,7 +378,7 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
           const bf16_t* rb = static_cast<const bf16_t*>(p.res) + col;
           uint2 raw[NQ];
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) raw[q] = *reinterpret_cast<const uint2*>(rb + rr[q] * p.ldr);
+          for (int q = 0; q < NQ; ++q) raw[q] = ldg8_nt(rb + rr[q] * p.ldr);
 #pragma unroll
           for (int q = 0; q < NQ; ++q) {
             res[q][0] = __uint_as_float(raw[q].x << 16);
@@ -384,15 +388,15 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
           }
         } else {
           const float* rf = static_cast<const float*>(p.res) + col;
-          float4 raw[NQ];
+          uint4 raw[NQ];
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) raw[q] = *reinterpret_cast<const float4*>(rf + rr[q] * p.ldr);
+          for (int q = 0; q < NQ; ++q) raw[q] = ldg16_nt(rf + rr[q] * p.ldr);
 #pragma unroll
           for (int q = 0; q < NQ; ++q) {
-            res[q][0] = raw[q].x;
-            res[q][1] = raw[q].y;
-            res[q][2] = raw[q].z;
-            res[q][3] = raw[q].w;
+            res[q][0] = __uint_as_float(raw[q].x);
+            res[q][1] = __uint_as_float(raw[q].y);
+            res[q][2] = __uint_as_float(raw[q].z);
+            res[q][3] = __uint_as_float(raw[q].w);
           }
         }
       }

@@ -70,8 +70,11 @@ hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const 
 hipError_t launch_saliency(int dtype_bf16, const void* x, const void* xref, const float* fw, int L, int N,
                            int D, double xi, float* s, double* num, double* den, double* step_delta,
                            hipStream_t stream);
+// with step_delta set, a second workgroup of the same launch writes the
+// step-level sum of num / den (the saliency pass's by-products)
 hipError_t launch_topk(const float* s, int L, int k, int threshold_mode, float threshold, int32_t* idx,
-                       uint8_t* mask, int32_t* n_sel, hipStream_t stream);
+                       uint8_t* mask, int32_t* n_sel, hipStream_t stream, const double* num = nullptr,
+                       const double* den = nullptr, double xi = 0.0, double* step_delta = nullptr);
 
 // two-stage selection (anchor segments, then min(k, N) tokens per anchor)
 hipError_t launch_topk_segments(const float* s, const uint8_t* anchors, int T, int N, int k, int32_t* idx,

@@ -88,10 +88,10 @@ saliency_rows(const T* __restrict__ x, const T* __restrict__ xref, const float* 
 }
 
 // Step-level Eq. 1 value sum(num) / (sum(den) + xi) in a fixed summation
-// order (deterministic): one 1024-thread workgroup.
-__global__ void __launch_bounds__(kSelThreads)
-step_delta_sum(const double* __restrict__ num, const double* __restrict__ den, int L, double xi,
-               double* __restrict__ step_delta) {
+// order (deterministic), by one 1024-thread workgroup: its own kernel after a
+// saliency-only call, or the second workgroup of the select_rows launch.
+__device__ __forceinline__ void step_delta_block(const double* __restrict__ num, const double* __restrict__ den,
+                                                 int L, double xi, double* __restrict__ step_delta) {
   __shared__ double red_n[kSelWaves], red_d[kSelWaves];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   double a = 0.0, b = 0.0;
@@ -117,6 +117,12 @@ step_delta_sum(const double* __restrict__ num, const double* __restrict__ den, i
     }
     *step_delta = sa / (sb + xi);
   }
+}
+
+__global__ void __launch_bounds__(kSelThreads)
+step_delta_sum(const double* __restrict__ num, const double* __restrict__ den, int L, double xi,
+               double* __restrict__ step_delta) {
+  step_delta_block(num, den, L, xi, step_delta);
 }
 
 // Order-preserving key: larger float -> larger key; NaN above everything; -0 == +0.
@@ -327,10 +333,18 @@ __device__ __forceinline__ void topk_rows(const float* __restrict__ s, int L, in
   if (tid == 0 && n_sel != nullptr) *n_sel = static_cast<int32_t>(base_sel);
 }
 
+// Workgroup 0 selects; workgroup 1 (launched only when step_delta is not
+// null) computes the step-level sum, independently of the selection.
 template <int R>
 __global__ void __launch_bounds__(kSelThreads)
 select_rows(const float* __restrict__ s, int L, int k, int threshold_mode, float threshold,
-            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel) {
+            int32_t* __restrict__ idx, uint8_t* __restrict__ mask, int32_t* __restrict__ n_sel,
+            const double* __restrict__ num, const double* __restrict__ den, double xi,
+            double* __restrict__ step_delta) {
+  if (blockIdx.x == 1) {
+    step_delta_block(num, den, L, xi, step_delta);
+    return;
+  }
   topk_rows<R>(s, L, k, threshold_mode, threshold, 0, idx, mask, n_sel);
 }
 
@@ -443,17 +457,19 @@ hipError_t launch_saliency(int dtype_bf16, const void* x, const void* xref, cons
 }
 
 hipError_t launch_topk(const float* s, int L, int k, int threshold_mode, float threshold, int32_t* idx,
-                       uint8_t* mask, int32_t* n_sel, hipStream_t stream) {
+                       uint8_t* mask, int32_t* n_sel, hipStream_t stream, const double* num,
+                       const double* den, double xi, double* step_delta) {
+  const dim3 grid(step_delta != nullptr ? 2 : 1);
 #define ECHO_SEL_CASE(RK)                                                                      \
   if (L <= RK * kSelThreads)                                                                   \
-    return ECHO_LAUNCH("select_rows", select_rows<RK>, dim3(1), dim3(kSelThreads), 0, stream, s, L, \
-                       k, threshold_mode, threshold, idx, mask, n_sel);
+    return ECHO_LAUNCH("select_rows", select_rows<RK>, grid, dim3(kSelThreads), 0, stream, s, L, \
+                       k, threshold_mode, threshold, idx, mask, n_sel, num, den, xi, step_delta);
   ECHO_SEL_CASE(8)
   ECHO_SEL_CASE(32)
   ECHO_SEL_CASE(80)
 #undef ECHO_SEL_CASE
-  return ECHO_LAUNCH("select_rows", select_rows<0>, dim3(1), dim3(kSelThreads), 0, stream, s, L, k,
-                     threshold_mode, threshold, idx, mask, n_sel);
+  return ECHO_LAUNCH("select_rows", select_rows<0>, grid, dim3(kSelThreads), 0, stream, s, L, k,
+                     threshold_mode, threshold, idx, mask, n_sel, num, den, xi, step_delta);
 }
 
 hipError_t launch_topk_segments(const float* s, const uint8_t* anchors, int T, int N, int k, int32_t* idx,
@@ -481,9 +497,10 @@ hipError_t launch_select(int dtype_bf16, const void* x, const void* xref, const 
                          int D, double xi, int k, int threshold_mode, float threshold, float* s,
                          double* num, double* den, int32_t* idx, uint8_t* mask, int32_t* n_sel,
                          double* step_delta, hipStream_t stream) {
-  const hipError_t e = launch_saliency(dtype_bf16, x, xref, fw, L, N, D, xi, s, num, den, step_delta, stream);
+  // the step-level sum runs beside the selection, in the same launch
+  const hipError_t e = launch_saliency(dtype_bf16, x, xref, fw, L, N, D, xi, s, num, den, nullptr, stream);
   if (e != hipSuccess) return e;
-  return launch_topk(s, L, k, threshold_mode, threshold, idx, mask, n_sel, stream);
+  return launch_topk(s, L, k, threshold_mode, threshold, idx, mask, n_sel, stream, num, den, xi, step_delta);
 }
 
 }  // namespace echo
