@@ -190,6 +190,9 @@ energy_reduce(const double* __restrict__ part, int T, int max_frames, int n_band
     const int t = i / n_bands, band = i % n_bands;
     const double* src = part + static_cast<int64_t>(t) * max_frames * n_bands + band;
     double acc = 0.0;
+    // unrolled so that eight frames' loads are in flight; the additions keep
+    // frame order
+#pragma unroll 8
     for (int f = 0; f < max_frames; ++f) acc += src[static_cast<int64_t>(f) * n_bands];
     bsum[i] = acc;
     band_energy[i] = static_cast<float>(acc);
