@@ -463,6 +463,12 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   const int tail = tiles % ncu;
   int nsplit = tail > 0 ? ncu / tail : 1;
   nsplit = nsplit < nk ? nsplit : nk;
+  // Each split also writes and the reduce reads a 256 KB fp32 partial tile:
+  // below about 20 k-steps per split that costs more than the shorter range
+  // saves (160 k-steps: 8 splits beat 16 by 7-11 us; 432: 16 beat 8).
+  constexpr int kMinStepsPerSplit = 20;
+  const int cap = nk / kMinStepsPerSplit > 1 ? nk / kMinStepsPerSplit : 1;
+  nsplit = nsplit < cap ? nsplit : cap;
   const size_t unit_bytes = sizeof(float) * BM * BN;
   while (nsplit > 1 && static_cast<size_t>(tail) * nsplit * unit_bytes > a.part_bytes) --nsplit;
   if (a.part == nullptr) nsplit = 1;
