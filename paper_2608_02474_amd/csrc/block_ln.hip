@@ -1,8 +1,10 @@
 // Modulated LayerNorm of token rows (the adaLN "LN(z) * (1 + scale) + shift"
 // in front of attention and FFN of the DiT block, Sec. 3.3).
 //
-// One wave per row; the row is held in registers (8-element chunks, all loads
-// issued before the first is used), mean and biased variance are reduced in
+// One wave per row; the row is held in registers (8-element chunks, all
+// non-temporal loads issued before the first is used; the output keeps
+// ordinary stores, since the GEMM after it reads it), mean and biased
+// variance are reduced in
 // fp32 with two passes over the registers, and the modulated result is
 // written in the output storage type.  Every access, the modulation vectors
 // included, is a 16-byte vector load or store.  Rows longer than 512 * MAXC

@@ -8,7 +8,8 @@
 //                           := x_i, output := cast(y_sel[j]);
 //   waves [n_sel, n_sel+L)  row i = wave - n_sel, if mask[i] == 0: output :=
 //                           cast(xref_i + scale_i * code).
-// Rows are streamed with 16-byte loads/stores (8 elements per chunk), every
+// Rows are streamed with 16-byte non-temporal loads/stores (8 elements per
+// chunk; nothing written here is read again before the next step), every
 // load of a row issued before the first is used; the fresh row's y and x stay
 // in registers between the absmax and the quantization.
 // Every fp32 step is a separately rounded IEEE operation (no fused

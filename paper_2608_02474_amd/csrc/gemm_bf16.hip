@@ -12,13 +12,15 @@
 // every lane feeds 8 consecutive k values (16 bytes).
 //
 // Tiling for gfx950: a BM x BN output tile per workgroup of WM x WN waves,
-// each wave (BM/WM) x (BN/WN) as 32x32 blocks of v_mfma_f32_32x32x16_bf16,
-// k-step 64.  A and B tiles are copied straight from global memory into a
-// double-buffered LDS ring with direct global-to-LDS loads (no VGPR staging;
-// each lane fetches the 16-byte piece whose swizzled slot is its lane slot),
-// one barrier per k-step.  LDS rows are 128 bytes; the 16-byte chunk of row r
-// is XOR-swizzled by (r >> 1) & 7 so that the 16 rows one LDS cycle reads
-// (two rows per 256-byte bank window) hit 16 distinct bank groups.
+// each wave (BM/WM) x (BN/WN) as 32x32 blocks of v_mfma_f32_32x32x16_bf16.
+// The build uses 256 x 256 tiles, 2 x 4 waves and a k-step of 32.  A and B
+// tiles are copied straight from global memory into an NS-stage LDS ring
+// (4 stages) with direct global-to-LDS loads (no VGPR staging; each lane
+// fetches the 16-byte piece whose swizzled slot is its lane slot), one
+// barrier per k-step.  LDS rows are BK * 2 bytes; the 16-byte chunk of row r
+// is XOR-swizzled (by (r >> 2) & 3 for 64-byte rows, (r >> 1) & 7 for
+// 128-byte rows) so that the rows one LDS cycle reads hit distinct bank
+// groups.
 // Workgroup ids are remapped so that each XCD (blocks are dealt round-robin
 // to the 8 XCDs) owns a contiguous run of tiles, then grouped 8 tile-rows at
 // a time so a run shares A and B panels in its L2.

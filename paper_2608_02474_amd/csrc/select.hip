@@ -1,12 +1,14 @@
 // Saliency and recompute selection (Sec. 3.1 Eq. 1, applied per token against
 // its cached input; Sec. 3.3 saliency mask with k = ceil(r L) tokens).
 //
-// saliency_rows: one wave per token row loads x and xref with 16-byte loads
-//   (all of a lane's loads issued before the first is used) and accumulates
+// saliency_rows: one wave per token row loads x and xref with 16-byte
+//   non-temporal loads (all of a lane's loads issued before the first is
+//   used) and accumulates
 //   |x - xref| and |xref| in fp64 (exact per-element differences, so only the
 //   summation order differs from the definition).
 //   Writes s_i = fp32(w_frame * num / (den + xi)) plus num/den for the step sum.
-// step_delta_sum: step-level Eq. 1 sum in a fixed order (deterministic).
+// step_delta_sum: step-level Eq. 1 sum in a fixed order (deterministic); in
+//   echo_select the same sum runs as a second workgroup of select_rows.
 // select_rows: one 1024-thread workgroup, the keys held in registers
 //   (1) top-K threshold key by 4-pass 8-bit radix select over order-preserving
 //       uint32 keys (histograms in LDS);
