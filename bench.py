@@ -347,14 +347,14 @@ def variants_leg(w, dev, dt, fe, fw, blocks, steps: int, n_anchor: int = 14, n_f
     am = api.anchors(T, n_anchor, "random", keys=keys)
     for _ in range(3):
         api.topk_segments(sel, am, N, kseg)
-        api.topk(sel, N, D, dt, k=n_anchor * kseg)
+        api.topk(sel, N, D, dt, k=api.segments_count(n_anchor, N, kseg))
     torch.cuda.synchronize()
     api.profile_enable(True)
     api.profile_read()
     for _ in range(20):
         api.anchors(T, n_anchor, "random", keys=keys, out=am)
         api.topk_segments(sel, am, N, kseg)
-        api.topk(sel, N, D, dt, k=n_anchor * kseg)
+        api.topk(sel, N, D, dt, k=api.segments_count(n_anchor, N, kseg))
     avgs = _kernel_avgs(api.profile_read())
     api.profile_enable(False)
     out["selection_kernels"] = {"anchors": n_anchor, "tokens_per_anchor": kseg,
@@ -377,9 +377,12 @@ def variants_leg(w, dev, dt, fe, fw, blocks, steps: int, n_anchor: int = 14, n_f
         ("all_full", dict(scheduler=api.Scheduler(steps, 1.0, 1.0, 0.0))),
         ("echocache", dict(scheduler=sched())),
         ("unit_frame_weight", dict(scheduler=sched(), fw=unit)),
-        ("two_stage_energy", dict(scheduler=sched(), anchor_mask=anchor_masks["energy"])),
-        ("two_stage_uniform", dict(scheduler=sched(), anchor_mask=anchor_masks["uniform"])),
-        ("two_stage_random", dict(scheduler=sched(), anchor_mask=anchor_masks["random"])),
+        ("two_stage_energy", dict(scheduler=sched(), anchor_mask=anchor_masks["energy"],
+                                     n_anchors=n_anchor)),
+        ("two_stage_uniform", dict(scheduler=sched(), anchor_mask=anchor_masks["uniform"],
+                                     n_anchors=n_anchor)),
+        ("two_stage_random", dict(scheduler=sched(), anchor_mask=anchor_masks["random"],
+                                     n_anchors=n_anchor)),
         ("step_only", dict(scheduler=api.Scheduler.step_only(n_full, refresh))),
         ("latent_only", dict(scheduler=api.Scheduler.latent_only(n_full, w.ratio))),
         ("fp16_cache", dict(scheduler=sched(), codec="full")),
@@ -398,7 +401,7 @@ def variants_leg(w, dev, dt, fe, fw, blocks, steps: int, n_anchor: int = 14, n_f
         two = cfg.get("anchor_mask") is not None
         cached = [e for e, (_, full, _) in zip(errs, stack.history) if not full]
         runs[name] = {"trajectory_ms": round(sum(times), 1),
-                      "tokens_recomputed": int(sum(L if full else (n_anchor * min(k, N) if two else k)
+                      "tokens_recomputed": int(sum(L if full else (api.segments_count(n_anchor, N, k) if two else k)
                                                    for k, full, _ in stack.history)),
                       "full_steps": int(sum(full for _, full, _ in stack.history)),
                       "cache_bytes_per_block": stack.cache_bytes() // len(blocks),

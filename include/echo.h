@@ -173,6 +173,25 @@ int echo_anchors(const float* keys, int32_t T, int32_t k, int32_t mode, uint8_t*
 int echo_topk_segments(const float* saliency, const uint8_t* anchors, int32_t T, int32_t N, int32_t k,
                        int32_t* idx, uint8_t* mask, int32_t* n_sel, void* stream);
 
+/* ------------------------------------------------------------ token counts */
+/*
+ * Host functions (no device work) that fix how many tokens a step recomputes.
+ *
+ * echo_topk_count: K = ceil(ratio * L - 1e-9), clamped to [0, L] -- the
+ * paper's k_t = ceil(N r_t) (Sec. 3.3, "Energy-Guided Step-Latent Cache
+ * Scheduling") taken over all L tokens of the step (global top-K).  The
+ * offset keeps products that are exact in decimal, such as 0.4 * 32760, from
+ * rounding up through their binary representation.  Returns K, or
+ * -ECHO_EINVAL for L < 1 or a ratio outside [0, 1] (NaN included).
+ *
+ * echo_segments_count: the number of tokens echo_topk_segments selects when
+ * n_anchors segments of N tokens are anchors and k tokens are requested per
+ * anchor segment: n_anchors * min(k, N).  Returns it, or -ECHO_EINVAL for
+ * n_anchors < 0, N < 1, k < 0 or a count of 2^31 or more.
+ */
+int32_t echo_topk_count(double ratio, int32_t L);
+int32_t echo_segments_count(int32_t n_anchors, int32_t N, int32_t k);
+
 /* ---------------------------------------------------------- step schedule */
 /*
  * Step-level cache schedule (Sec. 3.3, "Energy-Guided Step-Latent Cache
@@ -183,7 +202,7 @@ int echo_topk_segments(const float* saliency, const uint8_t* anchors, int32_t T,
  *                                     -> full step, acc = 0 (Eq. 2 refresh);
  *   otherwise dmax = max(dmax, delta_t); dhat = delta_t / dmax (0 if dmax == 0);
  *             r = clip(r_min + alpha * dhat, r_min, r_max);
- *             k = ceil(r * L - 1e-9), clamped to [0, L].
+ *             k = echo_topk_count(r, L).
  * delta_t is the step's Eq. 1 value (echo_saliency's step_delta); it is not
  * used on the leading full steps.  Returns k, or -ECHO_EINVAL for a bad
  * argument (L < 1, r_min > r_max, a rate outside [0, 1], NULL pointers).

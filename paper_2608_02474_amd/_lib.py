@@ -103,6 +103,8 @@ _SIGNATURES = {
     "echo_anchors": (ctypes.c_int, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
     "echo_topk_segments": (ctypes.c_int, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
                                           c_void_p, c_void_p, c_void_p]),
+    "echo_topk_count": (c_int32, [c_double, c_int32]),
+    "echo_segments_count": (c_int32, [c_int32, c_int32, c_int32]),
     "echo_schedule_next": (c_int32, [_P(ScheduleCfg), _P(ScheduleState), c_double, c_int32,
                                      _P(c_int32)]),
     "echo_block_workspace": (c_size_t, [_P(BlockCfg), c_int32]),

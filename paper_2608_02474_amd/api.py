@@ -15,7 +15,6 @@ from __future__ import annotations
 
 import ctypes
 import dataclasses
-import math
 
 import torch
 
@@ -284,21 +283,25 @@ class BlockStack:
 
     anchor_mask (uint8 [T] on the device, from `anchors`) switches to the
     two-stage selection: k_t = ceil(N r_t) tokens per anchor segment, ranked
-    by the saliency with unit frame weights.  codec: "residual_int8" (the
-    default), "full" (the outputs in the activation dtype) or "naive_int8"."""
+    by the saliency with unit frame weights; n_anchors is the number of
+    anchor segments it marks (the k given to `anchors`).  codec:
+    "residual_int8" (the default), "full" (the outputs in the activation
+    dtype) or "naive_int8"."""
 
     CODECS = {"residual_int8": 0, "full": 1, "naive_int8": 2}
 
     def __init__(self, params: list, H: int, L: int, D: int, device, dtype, scheduler: Scheduler,
                  xi: float = 1e-6, ln_eps: float = 1e-6, anchor_mask: torch.Tensor | None = None,
-                 codec: str = "residual_int8"):
+                 n_anchors: int | None = None, codec: str = "residual_int8"):
         if scheduler.cfg.n_full < 1:
             raise ValueError("the first step must be a full step (n_full >= 1)")
+        if (anchor_mask is None) != (n_anchors is None):
+            raise ValueError("pass anchor_mask and n_anchors together")
         if codec not in self.CODECS:
             raise ValueError(f"codec must be one of {tuple(self.CODECS)}")
         self.params, self.H, self.L, self.D = params, H, L, D
         self.sched, self.xi, self.ln_eps = scheduler, xi, ln_eps
-        self.anchor_mask, self.codec = anchor_mask, self.CODECS[codec]
+        self.anchor_mask, self.n_anchors, self.codec = anchor_mask, n_anchors, self.CODECS[codec]
         kw = dict(device=device)
         full = self.codec == self.CODECS["full"]
         self.xref = [torch.zeros((L, D), dtype=dtype, **kw) for _ in params]
@@ -311,7 +314,7 @@ class BlockStack:
         self.all_mask = torch.ones(L, dtype=torch.uint8, **kw)
         self._w = [block_weights(p) for p in params]
         self.ws, self.sel_ws, self.sel = Workspace(), Workspace(), None
-        self._unit, self._anchor_count = None, None
+        self._unit = None
         self.history = []   # (k, full, delta_t) per step; k per segment in the two-stage form
 
     def step(self, x0: torch.Tensor, frame_weight: torch.Tensor, N: int) -> torch.Tensor:
@@ -329,7 +332,7 @@ class BlockStack:
         elif two_stage:
             # the count is fixed by k and the anchors: no device read-back
             topk_segments(self.sel, self.anchor_mask, N, k)
-            idx, mask, n = self.sel.idx, self.sel.mask, self._n_anchor * min(k, N)
+            idx, mask, n = self.sel.idx, self.sel.mask, segments_count(self.n_anchors, N, k)
         else:
             topk(self.sel, N, self.D, x0.dtype, k=k)
             idx, mask, n = self.sel.idx, self.sel.mask, k
@@ -342,12 +345,6 @@ class BlockStack:
         self.history.append((k, full, delta_t))
         return x
 
-    @property
-    def _n_anchor(self) -> int:
-        if self._anchor_count is None:
-            self._anchor_count = int(self.anchor_mask.sum().item())   # once per clip
-        return self._anchor_count
-
     def cache_bytes(self) -> int:
         """Device bytes of the per-block cache state (saliency reference,
         codes and scales or the 16-bit store)."""
@@ -356,9 +353,19 @@ class BlockStack:
 
 
 def topk_count(ratio: float, L: int) -> int:
-    """K = ceil(r L), clamped to [0, L]; the small offset keeps exact products
-    such as 0.4 * 32760 from rounding up."""
-    return min(L, max(0, math.ceil(ratio * L - 1e-9)))
+    """K for a recompute ratio (echo_topk_count: ceil(r L), clamped to [0, L])."""
+    k = _lib_handle().echo_topk_count(float(ratio), int(L))
+    if k < 0:
+        check("echo_topk_count", -k)
+    return int(k)
+
+
+def segments_count(n_anchors: int, N: int, k: int) -> int:
+    """Tokens the two-stage selection recomputes (echo_segments_count)."""
+    n = _lib_handle().echo_segments_count(int(n_anchors), int(N), int(k))
+    if n < 0:
+        check("echo_segments_count", -n)
+    return int(n)
 
 
 # ------------------------------------------------------------- block partial

@@ -351,6 +351,18 @@ int echo_topk_segments(const float* saliency, const uint8_t* anchors, int32_t T,
       launch_topk_segments(saliency, anchors, T, N, k, idx, mask, n_sel, static_cast<hipStream_t>(stream)));
 }
 
+int32_t echo_topk_count(double ratio, int32_t L) {
+  if (L < 1 || !(ratio >= 0.0 && ratio <= 1.0)) return -ECHO_EINVAL;
+  const double kk = std::ceil(ratio * L - 1e-9);
+  return kk < 0.0 ? 0 : (kk > L ? L : static_cast<int32_t>(kk));
+}
+
+int32_t echo_segments_count(int32_t n_anchors, int32_t N, int32_t k) {
+  if (n_anchors < 0 || N < 1 || k < 0) return -ECHO_EINVAL;
+  const int64_t n = static_cast<int64_t>(n_anchors) * (k < N ? k : N);
+  return n >= (int64_t(1) << 31) ? -ECHO_EINVAL : static_cast<int32_t>(n);
+}
+
 int32_t echo_schedule_next(const echo_schedule_cfg* cfg, echo_schedule_state* st, double delta_t, int32_t L,
                            int32_t* full) {
   if (cfg == nullptr || st == nullptr || full == nullptr || L < 1 || cfg->n_full < 0 ||
@@ -373,9 +385,8 @@ int32_t echo_schedule_next(const echo_schedule_cfg* cfg, echo_schedule_state* st
   const double dhat = st->delta_max > 0.0 ? delta_t / st->delta_max : 0.0;
   double r = cfg->r_min + cfg->alpha * dhat;
   r = r < cfg->r_min ? cfg->r_min : (r > cfg->r_max ? cfg->r_max : r);
-  const double kk = std::ceil(r * L - 1e-9);
   *full = 0;
-  return kk < 0.0 ? 0 : (kk > L ? L : static_cast<int32_t>(kk));
+  return echo_topk_count(r, L);
 }
 
 size_t echo_block_workspace(const echo_block_cfg* cfg, int32_t n_sel_max) {

@@ -218,6 +218,7 @@ def _stack_variant(w, n_blocks, steps, sched, anchors=None, codec=OV.CODEC_RESID
                            api.Scheduler(sched.n_full, sched.r_min, sched.r_max, sched.alpha,
                                          sched.refresh_delta),
                            anchor_mask=None if anchors is None else up(anchors.astype(np.uint8)),
+                           n_anchors=None if anchors is None else int(np.count_nonzero(anchors)),
                            codec=CODEC_NAMES[codec])
     for t, x in enumerate(xs):
         y = stack.step(up(x, dt), up(fw), w.N)

@@ -38,6 +38,23 @@ def test_roundtrip_error_bound_and_symmetry():
     assert np.array_equal(c2, -codes) and np.array_equal(s2, scale)
 
 
+def test_codes_within_one_of_the_exact_definition():
+    """The fp32 operation order that decides the codes stays within one code
+    of the plain definition rint(res * 127 / amax) evaluated in fp64, and the
+    scale within an fp32 rounding of amax / 127."""
+    rng = np.random.default_rng(4)
+    res = (rng.standard_normal((256, 513)) * rng.uniform(1e-6, 1e3, size=(256, 1))).astype(np.float32)
+    res[::7, ::3] = 0.0
+    res[5] = np.float32(1.0) / np.arange(1, 514, dtype=np.float32)     # many codes near .5
+    codes, scale = C.quantize_rows(res)
+    r64 = res.astype(np.float64)
+    amax = np.abs(r64).max(axis=1, keepdims=True)
+    exact = np.clip(np.rint(r64 * 127.0 / amax), -127, 127)
+    assert (np.abs(codes.astype(np.int64) - exact) <= 1).all()
+    assert np.mean(codes == exact) > 0.999
+    assert np.allclose(scale.astype(np.float64), amax[:, 0] / 127.0, rtol=2 ** -23, atol=0)
+
+
 def test_zero_and_one_hot_rows():
     z = np.zeros((2, 10), np.float32)
     z[1, 4] = -3.5

@@ -59,3 +59,34 @@ def test_schedule_rejects_bad_arguments(lib):
     assert lib.echo_schedule_next(ctypes.byref(ok), ctypes.byref(st), 0.5, 0,
                                   ctypes.byref(full)) == -_lib.ECHO_EINVAL
     assert st.step == 0                                     # rejected calls leave the state alone
+
+
+def test_topk_count_matches_oracle(lib):
+    """echo_topk_count (the K the host passes to the top-K) against the
+    oracle's count: every workload's K, the sweep ratios, random ratios."""
+    import synth
+    from oracle.select import topk_count
+    for w in synth.ALL.values():
+        assert lib.echo_topk_count(w.ratio, w.L) == w.K == topk_count(w.ratio, w.L)
+    for r in synth.SWEEP_RATIOS:
+        assert lib.echo_topk_count(r, 32760) == topk_count(r, 32760)
+    rng = np.random.default_rng(3)
+    for _ in range(2000):
+        L = int(rng.integers(1, 200000))
+        r = float(rng.choice([rng.random(), round(rng.random(), 2), 0.0, 1.0]))
+        assert lib.echo_topk_count(r, L) == topk_count(r, L), (r, L)
+    assert lib.echo_topk_count(0.01, 10) == 1                 # ceil, not round
+    for bad in (-0.1, 1.01, float("nan")):
+        assert lib.echo_topk_count(bad, 10) == -_lib.ECHO_EINVAL
+    assert lib.echo_topk_count(0.5, 0) == -_lib.ECHO_EINVAL
+
+
+def test_segments_count(lib):
+    assert lib.echo_segments_count(14, 1560, 624) == 14 * 624
+    assert lib.echo_segments_count(14, 1560, 5000) == 14 * 1560     # at most N per segment
+    assert lib.echo_segments_count(0, 1560, 10) == 0
+    assert lib.echo_segments_count(21, 1560, 0) == 0
+    assert lib.echo_segments_count(-1, 10, 1) == -_lib.ECHO_EINVAL
+    assert lib.echo_segments_count(1, 0, 1) == -_lib.ECHO_EINVAL
+    assert lib.echo_segments_count(1, 10, -1) == -_lib.ECHO_EINVAL
+    assert lib.echo_segments_count(65536, 65536, 65536) == -_lib.ECHO_EINVAL
