@@ -49,7 +49,8 @@ typedef enum {
   ECHO_EINVAL = 1,        /* null/misaligned pointer, size out of range, bad shape */
   ECHO_EUNSUPPORTED = 2,  /* well-formed but outside the supported shapes/dtypes   */
   ECHO_EWORKSPACE = 3,    /* workspace pointer null or smaller than required       */
-  ECHO_EDEVICE = 4        /* a HIP call failed; see echo_last_hip_error()          */
+  ECHO_EDEVICE = 4,       /* a HIP call failed; see echo_last_hip_error()          */
+  ECHO_ELIMIT = 5         /* size above the fixed limit of an allocation-free call */
 } echo_status;
 
 typedef enum { ECHO_F32 = 0, ECHO_BF16 = 1 } echo_dtype;
@@ -140,6 +141,28 @@ int echo_saliency(const echo_select_cfg* cfg, const void* x, const void* xref,
                   void* workspace, size_t workspace_bytes, void* stream);
 int echo_topk(const echo_select_cfg* cfg, const float* saliency, int32_t* idx, uint8_t* mask,
               int32_t* n_sel, void* stream);
+
+/*
+ * echo_select without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Arguments, outputs and results are exactly those of
+ * echo_select (bit-identical).  The scratch space echo_select takes from its
+ * workspace (fp64 per-token sums; the fp32 saliency when `saliency` is NULL)
+ * is instead a static device array of the library sized for
+ * ECHO_SELECT_NOALLOC_MAX_TOKENS tokens (2.5 MiB); every GPU the library runs
+ * on holds one copy of it until the process ends.  Its device address is
+ * looked up on the first call on each device.  The call allocates nothing and
+ * calls no hipMalloc or hipFree.  L = T*N above ECHO_SELECT_NOALLOC_MAX_TOKENS
+ * returns ECHO_ELIMIT before anything is launched.  Every call on one GPU uses
+ * that GPU's single array, and nothing in it needs to start at zero (each
+ * call writes every entry it reads): calls that overlap on one GPU (other
+ * streams, or threads without ordering between them) race for it and give
+ * undefined results; calls ordered on one stream are safe.
+ */
+#define ECHO_SELECT_NOALLOC_MAX_TOKENS 131072
+int echo_select_noalloc(const echo_select_cfg* cfg, const void* x, const void* xref,
+                        const float* frame_weight, int32_t* idx, uint8_t* mask, int32_t* n_sel,
+                        float* saliency, double* step_delta, void* stream);
 
 /* ------------------------------------------------ two-stage selection */
 /*

@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libecho.so")
 HEADER = os.path.join(HERE, "..", "include", "echo.h")
 
-ECHO_OK, ECHO_EINVAL, ECHO_EUNSUPPORTED, ECHO_EWORKSPACE, ECHO_EDEVICE = range(5)
+ECHO_OK, ECHO_EINVAL, ECHO_EUNSUPPORTED, ECHO_EWORKSPACE, ECHO_EDEVICE, ECHO_ELIMIT = range(6)
+ECHO_SELECT_NOALLOC_MAX_TOKENS = 131072
 ECHO_F32, ECHO_BF16 = 0, 1
 ECHO_BLOCK_BATCH_INVARIANT = 1
 ECHO_ANCHOR_TOPK, ECHO_ANCHOR_UNIFORM = 0, 1
@@ -96,6 +97,8 @@ _SIGNATURES = {
     "echo_select": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                    c_void_p]),
+    "echo_select_noalloc": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p,
+                                           c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
     "echo_saliency_workspace": (c_size_t, [_P(SelectCfg)]),
     "echo_saliency": (ctypes.c_int, [_P(SelectCfg), c_void_p, c_void_p, c_void_p, c_void_p,
                                      c_void_p, c_void_p, c_size_t, c_void_p]),

@@ -155,6 +155,41 @@ def select(x: torch.Tensor, xref: torch.Tensor, frame_weight: torch.Tensor, N: i
     return out
 
 
+def select_noalloc(x: torch.Tensor, xref: torch.Tensor, frame_weight: torch.Tensor, N: int,
+                   out: Selection, k: int | None = None, threshold: float | None = None,
+                   xi: float = 1e-6) -> Selection:
+    """select into caller-provided outputs (`out`, e.g. from a previous
+    select) through echo_select_noalloc: the library's static scratch instead
+    of a workspace, so the call allocates no device memory (at most
+    ECHO_SELECT_NOALLOC_MAX_TOKENS tokens)."""
+    lib = _lib_handle()
+    _dev(x, "x")
+    _dev(xref, "xref", x.dtype)
+    _dev(frame_weight, "frame_weight", torch.float32)
+    L, D = x.shape
+    if L % N:
+        raise ValueError("L must be a multiple of N")
+    if (k is None) == (threshold is None):
+        raise ValueError("pass exactly one of k and threshold")
+    for t, n, dt in ((out.idx, "idx", torch.int32), (out.mask, "mask", torch.uint8),
+                     (out.n_sel_dev, "n_sel", torch.int32)):
+        _dev(t, n, dt)
+        if t.numel() < (1 if n == "n_sel" else L):
+            raise ValueError(f"out.{n} is too small")
+    if out.saliency is not None and (_dev(out.saliency, "saliency", torch.float32).numel() < L):
+        raise ValueError("out.saliency is too small")
+    if out.step_delta is not None:
+        _dev(out.step_delta, "step_delta", torch.float64)
+    cfg = SelectCfg(L // N, N, D, _echo_dtype(x), -1 if k is None else int(k),
+                    0.0 if threshold is None else float(threshold), float(xi))
+    check("echo_select_noalloc",
+          lib.echo_select_noalloc(ctypes.byref(cfg), _ptr(x), _ptr(xref), _ptr(frame_weight), _ptr(out.idx),
+                                  _ptr(out.mask), _ptr(out.n_sel_dev), _ptr(out.saliency),
+                                  _ptr(out.step_delta), _stream()))
+    out.n_sel = None if k is None else int(k)
+    return out
+
+
 def saliency(x: torch.Tensor, xref: torch.Tensor, frame_weight: torch.Tensor, N: int,
              xi: float = 1e-6, out: Selection | None = None,
              workspace: Workspace | None = None) -> Selection:

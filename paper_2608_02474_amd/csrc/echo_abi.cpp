@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "../../include/echo.h"
@@ -78,7 +79,7 @@ using namespace echo;
 namespace {
 
 constexpr size_t kAlign = 256;
-inline size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+constexpr size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline bool ok_ptr(const void* p) { return p != nullptr && aligned16(p); }
 inline size_t esize(int dtype) { return dtype == ECHO_BF16 ? 2 : 4; }
@@ -116,6 +117,54 @@ bool select_cfg_ok(const echo_select_cfg* c) {
 size_t select_ws(const echo_select_cfg* c) {
   const size_t L = static_cast<size_t>(c->T) * c->N;
   return align_up(L * sizeof(float)) + 2 * align_up(L * sizeof(double));
+}
+
+int select_args_status(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
+                       const int32_t* idx, const uint8_t* mask, const int32_t* n_sel, const float* saliency,
+                       const double* step_delta) {
+  if (!select_cfg_ok(cfg)) return ECHO_EINVAL;
+  if (!ok_ptr(x) || !ok_ptr(xref) || !ok_ptr(frame_weight) || !ok_ptr(idx) || !ok_ptr(mask) ||
+      n_sel == nullptr)
+    return ECHO_EINVAL;
+  if ((saliency != nullptr && !aligned16(saliency)) ||
+      (step_delta != nullptr && (reinterpret_cast<uintptr_t>(step_delta) & 7u)))
+    return ECHO_EINVAL;
+  return ECHO_OK;
+}
+int select_launch(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
+                  int32_t* idx, uint8_t* mask, int32_t* n_sel, float* saliency, double* step_delta,
+                  void* workspace, void* stream);
+
+// ---- allocation-free selection: the workspace of echo_select for up to
+// ECHO_SELECT_NOALLOC_MAX_TOKENS tokens as a static device array.  Each GPU
+// holds its own copy; its address is looked up once per device (with that
+// device current) and kept, and only that address is handed to kernels: in
+// host code the array's name is not a device address.
+constexpr size_t kNoAllocScratchBytes =
+    align_up(ECHO_SELECT_NOALLOC_MAX_TOKENS * sizeof(float)) + 2 * align_up(ECHO_SELECT_NOALLOC_MAX_TOKENS * sizeof(double));
+__device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (ECHO_EDEVICE if the
+// lookup fails).
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return ECHO_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return device_status(e);
+    if (p == nullptr) return ECHO_EDEVICE;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ECHO_OK;
 }
 
 // ---- block
@@ -242,6 +291,7 @@ const char* echo_status_str(int status) {
     case ECHO_EUNSUPPORTED: return "unsupported shape or dtype";
     case ECHO_EWORKSPACE: return "workspace missing or too small";
     case ECHO_EDEVICE: return "HIP device error";
+    case ECHO_ELIMIT: return "size above the allocation-free limit";
     default: return "unknown status";
   }
 }
@@ -281,15 +331,31 @@ size_t echo_select_workspace(const echo_select_cfg* cfg) {
 int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
                 int32_t* idx, uint8_t* mask, int32_t* n_sel, float* saliency, double* step_delta,
                 void* workspace, size_t workspace_bytes, void* stream) {
-  if (!select_cfg_ok(cfg)) return ECHO_EINVAL;
-  if (!ok_ptr(x) || !ok_ptr(xref) || !ok_ptr(frame_weight) || !ok_ptr(idx) || !ok_ptr(mask) ||
-      n_sel == nullptr)
-    return ECHO_EINVAL;
-  if ((saliency != nullptr && !aligned16(saliency)) ||
-      (step_delta != nullptr && (reinterpret_cast<uintptr_t>(step_delta) & 7u)))
-    return ECHO_EINVAL;
+  const int bad = select_args_status(cfg, x, xref, frame_weight, idx, mask, n_sel, saliency, step_delta);
+  if (bad != ECHO_OK) return bad;
   const size_t need = select_ws(cfg);
   if (!ok_ptr(workspace) || workspace_bytes < need) return ECHO_EWORKSPACE;
+  return select_launch(cfg, x, xref, frame_weight, idx, mask, n_sel, saliency, step_delta, workspace, stream);
+}
+
+int echo_select_noalloc(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
+                        int32_t* idx, uint8_t* mask, int32_t* n_sel, float* saliency, double* step_delta,
+                        void* stream) {
+  const int bad = select_args_status(cfg, x, xref, frame_weight, idx, mask, n_sel, saliency, step_delta);
+  if (bad != ECHO_OK) return bad;
+  if (static_cast<int64_t>(cfg->T) * cfg->N > ECHO_SELECT_NOALLOC_MAX_TOKENS) return ECHO_ELIMIT;
+  void* ws = nullptr;
+  const int st = noalloc_scratch(&ws);
+  if (st != ECHO_OK) return st;
+  return select_launch(cfg, x, xref, frame_weight, idx, mask, n_sel, saliency, step_delta, ws, stream);
+}
+
+}  // extern "C"
+
+namespace {
+int select_launch(const echo_select_cfg* cfg, const void* x, const void* xref, const float* frame_weight,
+                  int32_t* idx, uint8_t* mask, int32_t* n_sel, float* saliency, double* step_delta,
+                  void* workspace, void* stream) {
   const int L = cfg->T * cfg->N;
   char* ws = static_cast<char*>(workspace);
   float* s_ws = reinterpret_cast<float*>(ws);
@@ -302,6 +368,9 @@ int echo_select(const echo_select_cfg* cfg, const void* x, const void* xref, con
                                      cfg->threshold, s, num, den, idx, mask, n_sel, step_delta,
                                      static_cast<hipStream_t>(stream)));
 }
+}  // namespace
+
+extern "C" {
 
 size_t echo_saliency_workspace(const echo_select_cfg* cfg) {
   if (!select_cfg_ok(cfg)) return 0;

@@ -74,6 +74,17 @@ def test_select_rejects_before_launch(lib):
     assert run(_lib.SelectCfg(2, 16, 64, 0, 3, 0.0, 1e-6), wsb=16) == _lib.ECHO_EWORKSPACE
 
 
+def test_select_noalloc_rejects_before_launch(lib):
+    def run(cfg, x=FAKE):
+        return lib.echo_select_noalloc(ctypes.byref(cfg), x, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None)
+    lim = _lib.ECHO_SELECT_NOALLOC_MAX_TOKENS
+    assert run(_lib.SelectCfg(2, lim // 2 + 1, 64, 0, 3, 0.0, 1e-6)) == _lib.ECHO_ELIMIT
+    assert run(_lib.SelectCfg(1, lim + 1, 64, 1, 3, 0.0, 1e-6)) == _lib.ECHO_ELIMIT
+    assert run(_lib.SelectCfg(2, 16, 64, 0, 33, 0.0, 1e-6)) == _lib.ECHO_EINVAL     # k > L
+    assert run(_lib.SelectCfg(2, 16, 64, 0, 3, 0.0, 1e-6), x=MISALIGNED) == _lib.ECHO_EINVAL
+    assert lib.echo_status_str(_lib.ECHO_ELIMIT) == b"size above the allocation-free limit"
+
+
 def test_block_rejects_before_launch(lib):
     w = _lib.BlockWeights(*([0x20000] * 13))
     def run(cfg, n=4, wsb=1 << 40, weights=w):
