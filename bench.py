@@ -9,10 +9,14 @@ the Wan2.2-S2V-14B-shaped block at 480p: 21 latent frames x 30 x 52 = 32760
 tokens, hidden 5120, 40 heads of 128, FFN 13824, recompute ratio 0.4 (13104
 tokens), 5.06 s of 16 kHz audio.
 
-Prints one JSON line: whole-step tokens/s (L / step time), the roofline of the
-dominant kernel measured with HIP events on the launch stream during the timed
-steps, a per-kernel table, and the CPU oracle's throughput on a bounded sample
-(rank 0, N = 1).  Side legs, outside the timed step: the adaptive reference
+Prints one JSON line: whole-step tokens/s (L / step time) from exactly
+`--steps` uninstrumented steps, the step-time median / p10 / p90 over at least
+50 further steps with the shader clock and board power sampled meanwhile, the
+dense block over every token (the speedup's denominator), the roofline of the
+dominant kernel and a per-kernel table from a separate run of the same steps
+in which the library records HIP events around every launch on its stream, and
+the CPU oracle's throughput on bounded samples (fp64, and its fp32 timing mode;
+rank 0, N = 1).  Side legs, outside the timed step: the adaptive reference
 cache (update time, live references and bytes), a scheduled multi-block stack
 over a denoising trajectory, and the module ablation's variants (anchor
 strategies, step-only / latent-only schedules, 16-bit and naive int8 caches:
@@ -88,6 +92,140 @@ def _fit_time(fn, r1: int, r2: int, full: int) -> float:
     return fixed + per_row * full
 
 
+class ClockSampler:
+    """Samples the GPU's shader clock (MHz) and socket power (W) from a host
+    thread while the GPU works, through amdsmi's GPU metrics (the SMU's
+    current clock of every XCD and its current socket power); summary() gives
+    means and ranges, or None where a reading is unavailable."""
+
+    def __init__(self, device_index: int = 0, period_s: float = 0.02):
+        import threading
+        self.dev, self.period = device_index, period_s
+        self.clk, self.avg_clk, self.pwr = [], [], []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    @staticmethod
+    def _num(v):
+        return float(v) if isinstance(v, (int, float)) and not isinstance(v, bool) else None
+
+    def _run(self):
+        try:
+            import amdsmi
+            import torch
+            handle = torch.cuda._get_amdsmi_handler(self.dev)
+        except Exception:
+            return
+        while not self._stop.is_set():
+            try:
+                m = amdsmi.amdsmi_get_gpu_metrics_info(handle)
+                xcd = [self._num(c) for c in (m.get("current_gfxclks") or [])
+                       if isinstance(m.get("current_gfxclks"), list)]
+                xcd = [c for c in xcd if c]
+                if xcd:
+                    self.clk.append(sum(xcd) / len(xcd))
+                elif self._num(m.get("current_gfxclk")):
+                    self.clk.append(self._num(m.get("current_gfxclk")))
+                if self._num(m.get("average_gfxclk_frequency")):
+                    self.avg_clk.append(self._num(m.get("average_gfxclk_frequency")))
+                p = self._num(m.get("current_socket_power")) or self._num(m.get("average_socket_power"))
+                if p:
+                    self.pwr.append(p)
+            except Exception:
+                pass
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._thread.join()
+
+    def summary(self):
+        def stats(v):
+            if not v:
+                return None
+            v = sorted(v)
+            return {"mean": round(sum(v) / len(v), 1), "min": round(v[0], 1), "max": round(v[-1], 1),
+                    "samples": len(v)}
+        return {"sclk_mhz": stats(self.clk), "avg_gfxclk_mhz": stats(self.avg_clk), "power_w": stats(self.pwr),
+                "source": "amdsmi GPU metrics: mean of the XCDs' current gfx clocks, the SMU's average "
+                          "gfx clock, current socket power"}
+
+
+def _percentiles(v):
+    import numpy as np
+    a = np.asarray(v, np.float64)
+    return {"n": int(a.size), "median": round(float(np.median(a)), 4),
+            "p10": round(float(np.percentile(a, 10)), 4), "p90": round(float(np.percentile(a, 90)), 4),
+            "mean": round(float(a.mean()), 4), "min": round(float(a.min()), 4), "max": round(float(a.max()), 4)}
+
+
+def _per_step_times(step, steps: int):
+    """Wall times of `steps` consecutive step() calls from HIP events on the
+    current stream (one event at every step boundary); (total ms, [ms])."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(steps):
+        step()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[-1]), [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+
+
+def cpu_baseline_fp32(w, p, x, xref, audio, rows: int = 1024):
+    """The oracle's steps in its fp32 timing mode (single-precision,
+    BLAS-threaded numpy) on the host: the all-row LN + K/V projection of the
+    whole step, `rows` selected rows through Q, attention over all L keys, O
+    and the FFN (extrapolated per row to K), and the saliency, top-K and
+    cache update of the whole step."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import block as OB
+    from oracle import cache as OC
+    from oracle import energy as OE
+    from oracle import select as OS
+
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    L, K = w.L, w.K
+    p32 = OB._f64(p, np.float32)
+    x32 = np.asarray(x, np.float32)
+    t = {}
+    t0 = time.perf_counter()
+    fw = OE.energy(audio, w.T, w.sample_rate, w.n_fft, w.hop, w.n_bands)[2]
+    t["energy"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    s = OS.saliency(x, xref, fw, w.N)[0]
+    t["saliency"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    idx = OS.select_topk(s, K)
+    t["topk"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    kv = OB.kv_projection(p32, x32, dt=np.float32)
+    t["ln_kv"] = time.perf_counter() - t0
+    r = min(rows, K)
+    t0 = time.perf_counter()
+    y_part = OB.block_partial(p32, x32, idx[:r], w.H, kv=kv, dt=np.float32)
+    t["selected_rows"] = (time.perf_counter() - t0) * K / r
+    del kv
+    y_sel = np.resize(y_part, (K, w.D)).astype(np.float32)
+    t0 = time.perf_counter()
+    OC.cache_update(x, idx, y_sel, xref, np.zeros((L, w.D), np.int8), np.zeros(L, np.float32), w.dtype)
+    t["cache_update"] = time.perf_counter() - t0
+    total = sum(t.values())
+    return {"value": L / total, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"fp32 timing mode of the oracle (single-precision BLAS-threaded numpy): the whole "
+                       f"step's energy, saliency, top-K, LN + K/V projection of all {L} rows and cache "
+                       f"update; {r} of the {K} selected rows through Q, attention over all {L} keys, O "
+                       f"and FFN, extrapolated per row"),
+            "step_seconds": total, "parts_seconds": {k_: round(v_, 3) for k_, v_ in t.items()}}
+
+
 def cpu_baseline(w, p, x, xref, audio):
     """The CPU oracle, as it stands, timed on bounded samples of the workload;
     each part is extrapolated to the full step from two sample sizes."""
@@ -129,7 +267,7 @@ def cpu_baseline(w, p, x, xref, audio):
                                np.zeros(r_cache, np.float32), w.dtype) * L / r_cache
     total = sum(t.values())
     return {"value": L / total, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": (f"fp64 numpy oracle: full audio energy; saliency of {r_sal} rows; a full "
+            "sample": (f"fp64 numpy oracle, extrapolated: full audio energy; saliency of {r_sal} rows; a full "
                        f"{L}-key top-{K}; LN + K/V projection of {r_kv} rows; {r_sel[0]} and "
                        f"{r_sel[1]} selected rows (Q, attention over all {L} keys, O, FFN); cache "
                        f"update of {r_cache} rows. Row-proportional parts are scaled by rows; the "
@@ -707,19 +845,37 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
 
+    # headline: exactly `steps` steps with no library instrumentation
+    log(f"timing {args.steps} steps")
+    total_ms, per_step = _per_step_times(step, args.steps)
+    ms = total_ms / args.steps
+
+    # the step-time distribution over at least 50 more steps, with the shader
+    # clock and board power sampled meanwhile (uninstrumented as well)
+    n_dist = max(50, args.steps)
+    log(f"step-time distribution: {n_dist} steps, clock and power sampled")
+    with ClockSampler(0) as clock:
+        _, dist = _per_step_times(step, n_dist)
+    clock_summary = clock.summary()
+
+    # the plain dense block over every token (no selection, no cache update):
+    # the denominator of the cached step's speedup
+    log(f"dense block: {args.steps} calls over all {w.L} tokens")
+
+    def dense():
+        api.block_partial(P, X, blk.all_idx, w.L, w.H, y_sel=blk.y_sel, workspace=blk.ws, _weights=blk._w)
+    dense()
+    dense_total, dense_steps = _per_step_times(dense, args.steps)
+    dense_ms = dense_total / args.steps
+
+    # per-kernel times from a separate, instrumented run of the same steps
+    log(f"per-kernel timing: {args.steps} instrumented steps")
     api.profile_enable(True)
     api.profile_read()                        # drop anything recorded so far
-    log(f"timing {args.steps} steps")
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    stop.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
+    inst_total, _ = _per_step_times(step, args.steps)
     ktimes = api.profile_read()
     api.profile_enable(False)
+    inst_ms = inst_total / args.steps
 
     work = roofline.kernel_work(w.L, w.K, w.D, w.F, b, w.n_samples)
     kernels = {}
@@ -727,7 +883,7 @@ def main() -> int:
         avg = total_ms / launches
         wk = roofline.work_of(name, work)
         entry = {"avg_ms": round(avg, 4), "launches": launches,
-                 "share": round(total_ms / (ms * args.steps), 4)}
+                 "share": round(total_ms / (inst_ms * args.steps), 4)}
         if wk is not None and wk[0] > 0:
             amount, kind = wk
             if kind == "flop":
@@ -764,6 +920,16 @@ def main() -> int:
                    "latent_frames": w.T, "grid": list(w.grid), "hidden": w.D, "heads": w.H,
                    "ffn": w.F, "audio_samples": w.n_samples},
         "recomputed_tokens_per_s": round(w.K / (ms * 1e-3), 1),
+        "step_ms": {"timed_steps": _percentiles(per_step), "distribution": _percentiles(dist),
+                    "instrumented_mean": round(inst_ms, 4),
+                    "note": "timed_steps: the headline's steps; distribution: max(50, steps) further "
+                            "uninstrumented steps; instrumented_mean: the per-kernel run with two HIP "
+                            "events per launch"},
+        "clock": dict(clock_summary, during="the distribution steps"),
+        "dense_block": {"ms": round(dense_ms, 4), "tokens_per_s": round(w.L / (dense_ms * 1e-3), 1),
+                        "tflops": round(roofline.block_flops(w.L, w.L, w.D, w.F) / (dense_ms * 1e-3) / 1e12, 2),
+                        "speedup_of_cached_step": round(dense_ms / ms, 3),
+                        "what": "echo_block_partial over all L tokens (no selection, no cache update)"},
         "roofline": roof,
         "block_partial": {"ms": round(block_ms, 4), "tflops": round(block_tf, 2),
                           "frac_bf16_peak": round(block_tf / roofline.PEAK_BF16_TFLOPS, 4)},
@@ -814,8 +980,10 @@ def main() -> int:
     if args.skip_cpu_baseline:
         out["cpu_baseline"] = None
     else:
-        log("CPU oracle baseline on a bounded sample")
+        log("CPU oracle baseline on a bounded sample (fp64)")
         out["cpu_baseline"] = cpu_baseline(w, p, x, xref, audio)
+        log("CPU oracle in its fp32 timing mode")
+        out["cpu_baseline"]["fp32_timing_mode"] = cpu_baseline_fp32(w, p, x, xref, audio)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -20,7 +20,10 @@ generators); its exact form is a reading:
 
 LN has no affine parameters, biased variance and eps = 1e-6; the modulation
 rows are (shift1, scale1, gate1, shift2, scale2, gate2), broadcast over tokens.
-Everything is fp64; weights are [out, in] (nn.Linear layout).
+Everything is fp64; weights are [out, in] (nn.Linear layout).  The partial
+block's functions also take `dt`, the floating type they compute in: fp64 for
+every parity check, fp32 only to time the same steps with single-precision
+BLAS on the host.
 """
 from __future__ import annotations
 
@@ -29,8 +32,8 @@ import numpy as np
 LN_EPS = 1e-6
 
 
-def layer_norm(z: np.ndarray, eps: float = LN_EPS) -> np.ndarray:
-    z = np.asarray(z, dtype=np.float64)
+def layer_norm(z: np.ndarray, eps: float = LN_EPS, dt=np.float64) -> np.ndarray:
+    z = np.asarray(z, dtype=dt)
     mu = z.mean(axis=-1, keepdims=True)
     var = ((z - mu) ** 2).mean(axis=-1, keepdims=True)
     return (z - mu) / np.sqrt(var + eps)
@@ -40,16 +43,16 @@ def gelu_tanh(z: np.ndarray) -> np.ndarray:
     return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
 
 
-def linear(a: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
-    return np.asarray(a, np.float64) @ np.asarray(w, np.float64).T + np.asarray(b, np.float64)
+def linear(a: np.ndarray, w: np.ndarray, b: np.ndarray, dt=np.float64) -> np.ndarray:
+    return np.asarray(a, dt) @ np.asarray(w, dt).T + np.asarray(b, dt)
 
 
-def _f64(p: dict) -> dict:
-    return {k: np.asarray(v, dtype=np.float64) for k, v in p.items()}
+def _f64(p: dict, dt=np.float64) -> dict:
+    return {k: np.asarray(v, dtype=dt) for k, v in p.items()}
 
 
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, H: int,
-              chunk: int = 1024) -> np.ndarray:
+              chunk: int = 1024, dt=np.float64) -> np.ndarray:
     """Multi-head attention of the rows of q over all rows of k, v.
 
     q [M, D], k and v [L, D]; head h uses columns h*dh .. (h+1)*dh.  The query
@@ -58,8 +61,8 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, H: int,
     """
     M, D = q.shape
     dh = D // H
-    out = np.empty((M, D), dtype=np.float64)
-    scale = 1.0 / np.sqrt(dh)
+    out = np.empty((M, D), dtype=dt)
+    scale = dt(1.0 / np.sqrt(dh))
     for h in range(H):
         cols = slice(h * dh, (h + 1) * dh)
         kh, vh = k[:, cols], v[:, cols]
@@ -72,30 +75,30 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, H: int,
     return out
 
 
-def kv_projection(p: dict, x: np.ndarray, eps: float = LN_EPS):
+def kv_projection(p: dict, x: np.ndarray, eps: float = LN_EPS, dt=np.float64):
     """Modulated LN of all rows and the key/value projections of all rows."""
     mod = p["mod"]
-    a = layer_norm(x, eps) * (1.0 + mod[1]) + mod[0]
-    return a, linear(a, p["wk"], p["bk"]), linear(a, p["wv"], p["bv"])
+    a = layer_norm(x, eps, dt) * (1.0 + mod[1]) + mod[0]
+    return a, linear(a, p["wk"], p["bk"], dt), linear(a, p["wv"], p["bv"], dt)
 
 
 def block_partial(params: dict, x: np.ndarray, idx: np.ndarray, H: int,
-                  eps: float = LN_EPS, kv=None) -> np.ndarray:
+                  eps: float = LN_EPS, kv=None, dt=np.float64) -> np.ndarray:
     """Block output for the selected rows idx only: y_sel [len(idx), D], fp64.
 
     `kv` optionally passes a precomputed (a, k, v) from kv_projection for the
     same x, so that several row samples can share the all-row projections.
     """
-    p = _f64(params)
-    x = np.asarray(x, dtype=np.float64)
+    p = _f64(params, dt)
+    x = np.asarray(x, dtype=dt)
     idx = np.asarray(idx, dtype=np.int64)
     mod = p["mod"]
-    a, k, v = kv_projection(p, x, eps) if kv is None else kv
-    q = linear(a[idx], p["wq"], p["bq"])
-    o = attention(q, k, v, H)
-    x1 = x[idx] + mod[2] * linear(o, p["wo"], p["bo"])
-    b = layer_norm(x1, eps) * (1.0 + mod[4]) + mod[3]
-    f = linear(gelu_tanh(linear(b, p["w1"], p["b1"])), p["w2"], p["b2"])
+    a, k, v = kv_projection(p, x, eps, dt) if kv is None else kv
+    q = linear(a[idx], p["wq"], p["bq"], dt)
+    o = attention(q, k, v, H, dt=dt)
+    x1 = x[idx] + mod[2] * linear(o, p["wo"], p["bo"], dt)
+    b = layer_norm(x1, eps, dt) * (1.0 + mod[4]) + mod[3]
+    f = linear(gelu_tanh(linear(b, p["w1"], p["b1"], dt)), p["w2"], p["b2"], dt)
     return x1 + mod[5] * f
 
 

@@ -154,7 +154,7 @@ def test_select_register_limit(grid):
 
 # -------------------------------------------------------------------- cache
 
-@pytest.mark.parametrize("w", [synth.TINY, RAGGED, synth.SMALL, synth.WAN14B_480P],
+@pytest.mark.parametrize("w", [synth.TINY, RAGGED, synth.SMALL, synth.WAN14B_480P, synth.WAN14B_720P],
                          ids=lambda w: w.name)
 def test_cache_update_bit_exact(w):
     say(f"cache {w.name}")
@@ -272,19 +272,41 @@ def test_block_gates_one_informational():
 _KV = {}
 
 
-def _kv_shared(w, p, x):
-    """The oracle's all-row LN + K/V projection of x, kept for the ratio cases
-    of one workload (it does not depend on the selection)."""
-    if w.name not in _KV:
-        _KV.clear()
-        _KV[w.name] = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
-    return _KV[w.name]
+def _kv_shared(w, p, x, tag="x"):
+    """The oracle's all-row LN + K/V projection of one input (`tag` names it),
+    kept for the tests of one workload (it does not depend on the selection);
+    at most two projections are held at a time."""
+    key = (w.name, tag)
+    if key not in _KV:
+        while len(_KV) >= 2:
+            _KV.pop(next(iter(_KV)))
+        _KV[key] = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    return _KV[key]
 
 
-@pytest.mark.parametrize("w", [synth.WAN14B_480P, synth.WAN14B_720P], ids=lambda w: w.name)
-def test_block_partial_full_size_sampled(w):
-    """Full-size block in the launch configuration the benchmark times; the
-    oracle computes the all-row K/V projection and then sampled rows."""
+ATTN_Q_TILE = 384   # queries of one attention workgroup
+GEMM_TILE = 256     # rows of one GEMM tile
+
+
+def _tile_rows(K, rng):
+    """Positions in the selection that the full-size tests compare: one from
+    every 384-query attention tile (each spans all heads, so the key-split
+    tail items of the last round are reached too), every row of the last
+    partial query tile, 16 rows of the last (partial) 256-row GEMM tile, and
+    the first and last rows."""
+    rows = [int(rng.integers(t, min(t + ATTN_Q_TILE, K))) for t in range(0, K, ATTN_Q_TILE)]
+    rows += list(range((K // ATTN_Q_TILE) * ATTN_Q_TILE, K))
+    last_g = ((K - 1) // GEMM_TILE) * GEMM_TILE
+    rows += rng.choice(np.arange(last_g, K), min(16, K - last_g), replace=False).tolist()
+    rows += [0, K - 1]
+    return np.unique(np.asarray(rows, np.int64))
+
+
+def test_block_partial_full_size_sampled():
+    """Full-size block (32760 tokens) in the launch configuration the
+    benchmark times; the oracle computes the all-row K/V projection and then
+    the rows of every query tile."""
+    w = synth.WAN14B_480P
     p = synth.make_block_weights(w)
     xref, x = synth.make_latents(w)
     fw = _frame_weight(w)
@@ -292,20 +314,17 @@ def test_block_partial_full_size_sampled(w):
     idx = OS.select_topk(s, w.K)
     say(f"block {w.name} K={w.K} (GPU)")
     got = _block_gpu(w, p, x, idx)
-    rng = np.random.default_rng(8)
-    rows = np.unique(np.concatenate([[0, w.K - 1, w.K // 2],
-                                     rng.choice(w.K, 29, replace=False)]))
-    say(f"block {w.name}: oracle on {len(rows)} sampled rows")
-    kv = _kv_shared(w, p, x) if w is synth.WAN14B_480P else None
-    want = OB.block_partial(p, x, idx[rows], w.H, kv=kv)
-    check_block(got[rows], want, w.dtype, f"{w.name}/sampled")
+    rows = _tile_rows(w.K, np.random.default_rng(8))
+    say(f"block {w.name}: oracle on {len(rows)} rows (every query tile)")
+    want = OB.block_partial(p, x, idx[rows], w.H, kv=_kv_shared(w, p, x))
+    check_block(got[rows], want, w.dtype, f"{w.name}/tile rows")
 
 
 @pytest.mark.parametrize("ratio", synth.SWEEP_RATIOS, ids=lambda r: f"r{r}")
 def test_block_partial_ratio_sweep_sampled(ratio):
     """The 32760-token block at every recompute ratio of the sweep (K from
     3276 to all 32760 tokens: other GEMM and attention grids and split tails
-    than the 0.4 case), sampled rows against the oracle."""
+    than the 0.4 case), the rows of every query tile against the oracle."""
     w = synth.WAN14B_480P.with_(ratio=ratio)
     p = synth.make_block_weights(w)
     xref, x = synth.make_latents(w)
@@ -314,12 +333,79 @@ def test_block_partial_ratio_sweep_sampled(ratio):
     idx = OS.select_topk(s, w.K)
     say(f"block {w.name} r={ratio} K={w.K} (GPU)")
     got = _block_gpu(w, p, x, idx)
-    rng = np.random.default_rng(10)
-    rows = np.unique(np.concatenate([[0, w.K - 1, w.K // 2],
-                                     rng.choice(w.K, 21, replace=False)]))
-    say(f"block r={ratio}: oracle on {len(rows)} sampled rows")
+    rows = _tile_rows(w.K, np.random.default_rng(10))
+    say(f"block r={ratio}: oracle on {len(rows)} rows (every query tile)")
     want = OB.block_partial(p, x, idx[rows], w.H, kv=_kv_shared(w, p, x))
-    check_block(got[rows], want, w.dtype, f"{w.name}/r{ratio}/sampled")
+    check_block(got[rows], want, w.dtype, f"{w.name}/r{ratio}/tile rows")
+
+
+@pytest.mark.parametrize("w", [synth.WAN14B_480P, synth.WAN14B_720P], ids=lambda w: w.name)
+def test_cached_step_end_to_end_full_size(w):
+    """One whole cached step at full size through CachedBlock (the benchmark's
+    calls and launch configuration), after the init step on xref:
+      - the init step stores xref itself as the reference;
+      - the selection equals the oracle's (ties within 1e-6 excluded);
+      - codes, scales, references and the fused output equal the oracle's
+        cache update bit for bit, given the GPU's fresh rows and init cache;
+      - fresh rows of every query tile equal the oracle block, over the tokens
+        both selections contain;
+      - reused rows are within the block bar plus one quantization step of
+        the oracle's own init-then-reuse output, and the init step's rows
+        (every token recomputed: the dense block) match the oracle."""
+    p = synth.make_block_weights(w)
+    xref, x = synth.make_latents(w)
+    fw = _frame_weight(w)
+    dt = tdtype(w.dtype)
+    L, K = w.L, w.K
+    rng = np.random.default_rng(12)
+    blk = api.CachedBlock(params_to_device(p, w.dtype), w.H, L, w.D, device(), dt)
+    say(f"step {w.name}: init on xref, then K={K} (GPU)")
+    blk.init(up(xref, dt))
+    torch.cuda.synchronize()
+    xref0, codes0, scale0 = down(blk.xref).copy(), down(blk.codes).copy(), down(blk.scale).copy()
+    # reused rows to check: a sample of tokens the oracle leaves unselected
+    s, _, _ = OS.saliency(x, xref, fw, w.N)
+    want_idx = OS.select_topk(s, K)
+    rest_o = np.setdiff1d(np.arange(L), want_idx)
+    reuse = np.sort(rng.choice(rest_o, 48, replace=False))
+    ys_init = down(blk.y_sel)[reuse].copy()
+    y = blk.step(up(x, dt), up(fw), w.N, k=K)
+    torch.cuda.synchronize()
+
+    assert np.array_equal(_bits(xref0), _bits(xref))
+    gi = down(blk.sel.idx)[:K].astype(np.int64)
+    nd = check_selection(gi, want_idx, s, K)
+    say(f"  selection: {nd} tie-excluded differences")
+
+    ys = down(blk.y_sel)[:K]
+    y_o, xr_o, c_o, s_o = OC.cache_update(x, gi, ys, xref0, codes0, scale0, w.dtype)
+    assert np.array_equal(down(blk.codes), c_o)
+    assert np.array_equal(_bits(down(blk.scale)), _bits(s_o))
+    assert np.array_equal(_bits(down(blk.xref)), _bits(xr_o))
+    gy = down(y)
+    assert np.array_equal(_bits(gy), _bits(y_o))
+    del y_o, xr_o, c_o, s_o
+    say("  cache state and fused output bit-exact")
+
+    pos = _tile_rows(K, rng)
+    pos = pos[np.isin(gi[pos], want_idx)]
+    say(f"  fresh rows: oracle on {len(pos)} rows (every query tile)")
+    want = OB.block_partial(p, x, gi[pos], w.H, kv=_kv_shared(w, p, x, "x"))
+    check_block(ys[pos], want, w.dtype, f"{w.name}/step fresh rows")
+
+    keep = ~np.isin(reuse, gi)                   # unselected on the GPU side too
+    reuse, ys_init = reuse[keep], ys_init[keep]
+    say(f"  reused rows: oracle init block on {len(reuse)} rows")
+    yi = OB.block_partial(p, xref, reuse, w.H, kv=_kv_shared(w, p, xref, "xref")).astype(np.float32)
+    check_block(ys_init, yi, w.dtype, f"{w.name}/init rows")
+    c_i, s_i = OC.quantize_rows((yi - xref[reuse]).astype(np.float32))
+    y_reuse_o = OC.cast_act(OC.dequantize_rows(xref[reuse], c_i, s_i), w.dtype)
+    tol = TOL_BF16_ABS if w.dtype == "bf16" else TOL_F32_ABS
+    sc = np.maximum(down(blk.scale)[reuse], s_i)[:, None]
+    cast = np.abs(y_reuse_o) * (2.0 ** -8 if w.dtype == "bf16" else 2.0 ** -23)
+    err = np.abs(gy[reuse].astype(np.float64) - y_reuse_o)
+    say(f"  reused rows: max|err| {err.max():.3e}")
+    assert (err <= tol + sc + cast).all(), float((err - (tol + sc + cast)).max())
 
 
 def test_block_row_independence_full_size():
@@ -366,12 +452,14 @@ def test_cached_step_end_to_end(w):
     y = blk.step(up(x, dt), up(fw), w.N, k=w.K)
     torch.cuda.synchronize()
     gi = down(blk.sel.idx)[: w.K]
-    check_selection(gi, o_step["idx"], o_step["s"], w.K)
-    same = np.array_equal(gi, o_step["idx"])
+    nd = check_selection(gi, o_step["idx"], o_step["s"], w.K)
     gy = down(y)
     tol = TOL_F32_ABS if w.dtype == "f32" else TOL_BF16_ABS
-    if same:
-        check_block(down(blk.y_sel)[: w.K], o_step["y_sel"], w.dtype, f"{w.name}/step y_sel")
+    # fresh rows over the tokens both selections contain (all of them unless a
+    # tie within 1e-6 of the K-th saliency went the other way)
+    both, g_pos, o_pos = np.intersect1d(gi, o_step["idx"], return_indices=True)
+    assert len(both) == w.K - nd // 2
+    check_block(down(blk.y_sel)[: w.K][g_pos], o_step["y_sel"][o_pos], w.dtype, f"{w.name}/step y_sel")
     # reused rows: each side dequantizes its own cache; allow the block tolerance,
     # one quantization step of either cache, and the final cast
     rest = np.setdiff1d(np.arange(w.L), gi)

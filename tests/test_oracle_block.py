@@ -110,3 +110,17 @@ def test_precomputed_kv_path_identical():
     idx = np.array([1, 2, 30])
     assert np.array_equal(B.block_partial(p, x, idx, TINY.H),
                           B.block_partial(p, x, idx, TINY.H, kv=kv))
+
+
+def test_fp32_timing_mode_matches_fp64():
+    """The fp32 mode (used only to time the oracle's steps with
+    single-precision BLAS) computes the same block within fp32 rounding."""
+    import synth
+    w = synth.TINY
+    p = synth.make_block_weights(w)
+    _, x = synth.make_latents(w)
+    idx = np.array([0, 5, 17, 31])
+    a = B.block_partial(p, x, idx, w.H)
+    b = B.block_partial(p, x, idx, w.H, dt=np.float32)
+    assert b.dtype == np.float32
+    assert np.abs(a - b).max() <= 1e-5 * max(1.0, np.abs(a).max())
