@@ -797,6 +797,8 @@ def main() -> int:
                     help="timed steps per (ratio, audio profile) of the ratio-sweep leg; 0: skip")
     ap.add_argument("--p720-steps", type=int, default=10,
                     help="timed steps of the 720p-shaped block leg; 0: skip")
+    ap.add_argument("--dist-steps", type=int, default=50,
+                    help="uninstrumented steps of the step-time distribution (at least --steps)")
     ap.add_argument("--skip-cpu-baseline", action="store_true",
                     help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
                          "unchanged")
@@ -852,7 +854,7 @@ def main() -> int:
 
     # the step-time distribution over at least 50 more steps, with the shader
     # clock and board power sampled meanwhile (uninstrumented as well)
-    n_dist = max(50, args.steps)
+    n_dist = max(args.dist_steps, args.steps)
     log(f"step-time distribution: {n_dist} steps, clock and power sampled")
     with ClockSampler(0) as clock:
         _, dist = _per_step_times(step, n_dist)
@@ -922,7 +924,7 @@ def main() -> int:
         "recomputed_tokens_per_s": round(w.K / (ms * 1e-3), 1),
         "step_ms": {"timed_steps": _percentiles(per_step), "distribution": _percentiles(dist),
                     "instrumented_mean": round(inst_ms, 4),
-                    "note": "timed_steps: the headline's steps; distribution: max(50, steps) further "
+                    "note": "timed_steps: the headline's steps; distribution: max(dist_steps, steps) further "
                             "uninstrumented steps; instrumented_mean: the per-kernel run with two HIP "
                             "events per launch"},
         "clock": dict(clock_summary, during="the distribution steps"),

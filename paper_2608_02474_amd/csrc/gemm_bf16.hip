@@ -11,19 +11,15 @@
 // Both operands are K-contiguous, which is what the MFMA operand layout wants:
 // every lane feeds 8 consecutive k values (16 bytes).
 //
-// Tiling for gfx950: a BM x BN output tile per workgroup of WM x WN waves,
-// each wave (BM/WM) x (BN/WN) as 32x32 blocks of v_mfma_f32_32x32x16_bf16.
-// The build uses 256 x 256 tiles, 2 x 4 waves and a k-step of 32.  A and B
-// tiles are copied straight from global memory into an NS-stage LDS ring
-// (4 stages) with direct global-to-LDS loads (no VGPR staging; each lane
-// fetches the 16-byte piece whose swizzled slot is its lane slot), one
-// barrier per k-step.  LDS rows are BK * 2 bytes; the 16-byte chunk of row r
-// is XOR-swizzled (by (r >> 2) & 3 for 64-byte rows, (r >> 1) & 7 for
-// 128-byte rows) so that the rows one LDS cycle reads hit distinct bank
-// groups.
+// Tiling for gfx950: 256 x 256 output tiles, one workgroup of four waves
+// (one per SIMD) per tile, each wave a 128 x 128 quarter as 8 x 8 blocks of
+// v_mfma_f32_16x16x32_bf16, k-steps of 64 through a two-stage LDS ring that
+// direct global-to-LDS copies fill (gemm_bf16_w4 below).
 // Workgroup ids are remapped so that each XCD (blocks are dealt round-robin
 // to the 8 XCDs) owns a contiguous run of tiles, then grouped 8 tile-rows at
-// a time so a run shares A and B panels in its L2.
+// a time so a run shares A and B panels in its L2.  Tiles that do not fill a
+// last round of the device are split along k (gemm_splitk_reduce adds the
+// ranges in order and applies the epilogue).
 // Requires N % BN == 0, n_split % BN == 0, K % BK == 0 and byte offsets of
 // A and B rows below 2^31; M is arbitrary (tail rows clamp their loads and
 // skip their stores).
@@ -34,15 +30,6 @@
 #include "launch.h"
 
 namespace echo {
-
-// LDS rows hold BK bf16 (BK/8 chunks of 16 B).  The chunk of row r is
-// XOR-swizzled so that the 16 consecutive rows one LDS cycle serves (256
-// bytes = 2 rows of 128 B, or 4 rows of 64 B) land in 16 distinct bank groups.
-template <int BK>
-__device__ __forceinline__ int gslot(int row, int chunk) {
-  if (BK == 64) return chunk ^ ((row >> 1) & 7);
-  return chunk ^ ((row >> 2) & 3);
-}
 
 // f(integral_constant<int, I>) for I = B .. E-1, unrolled at compile time
 template <int B, int E, typename F>
@@ -132,30 +119,47 @@ __device__ __forceinline__ void gemm_store4(const GemmBf16Args& p, int row, int 
   }
 }
 
-template <int BM, int BN, int WM, int WN, int NS, int BK>
-struct GemmCfg {
-  static constexpr int kWaves = WM * WN;
-  static constexpr int kThreads = kWaves * 64;
-  static constexpr int kTM = BM / WM / 32;                 // 32x32 blocks per wave (rows)
-  static constexpr int kTN = BN / WN / 32;                 // (columns)
-  static constexpr int kRowBytes = BK * 2;
-  static constexpr int kRowsPerCopy = 1024 / kRowBytes;     // rows one 1 KB copy fills
-  static constexpr int kStageBytes = (BM + BN) * kRowBytes;  // A + B tiles
-  static constexpr int kCopies = (BM + BN) / kRowsPerCopy / kWaves;  // per wave per k-step
-  static_assert(BK == 32 || BK == 64, "k-step of 32 or 64");
-  static_assert((BM + BN) % (kRowsPerCopy * kWaves) == 0, "copies split evenly over the waves");
-  static_assert(BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tile of 32x32 blocks");
-  static_assert(NS >= 2 && NS <= 5 && NS * kStageBytes <= 160 * 1024, "LDS ring fits");
-};
+// ---- the tile kernel.  Each wave owns a 128 x 128 quarter of the tile as
+// 8 x 8 blocks of v_mfma_f32_16x16x32_bf16 (accumulators: 256 AGPRs per lane;
+// fragments of two k32 halves in flight: 128 VGPRs).  The LDS holds two
+// stages of 64 KB (A ++ B, 512 rows of 128 bytes; the 16-byte chunk of row r
+// is XOR-swizzled by (r >> 1) & 7, so that the 16 rows one LDS cycle serves
+// hit 16 distinct bank groups).  A k-step is
+//   (0)  the 64 MFMAs of its first k32 half, with the 16 fragment reads of
+//        the second half and the last 8 copies of the k-step after next
+//        between them (one read per four MFMAs, one copy per four MFMAs over
+//        the first 32);
+//   (1a) 32 MFMAs of the second half;
+//   --   a wait for this wave's copies of the next k-step and a barrier:
+//        after it the next stage is complete everywhere and no wave reads
+//        the current one any more (its fragments are all in registers);
+//   (1b) the last 32 MFMAs, with the 16 reads of the next k-step's first half
+//        and the first 8 copies of the k-step after next into the stage just
+//        released.
+// A copy thus has about one k-step to land, and a k-step's only wait sits
+// between MFMAs.  The loop runs from one barrier to the next ((1b) of k-step
+// kt, then (0) and (1a) of kt + 1), so every fragment read is used in the
+// iteration that issues it and the compiler's wait counts stay exact.  Past
+// the last k-step the copies re-fetch it (in bounds, never read).  Against
+// the earlier 8-wave form (32x32x16 MFMAs, 128 x 64 per wave, a four-stage
+// ring of k32 steps) this reads a third fewer LDS bytes per MFMA and keeps
+// the MFMA pipes busier: K/V projection 2.90 -> 2.46 ms, FFN 1.66 -> 1.45 ms.
+constexpr int kW4Threads = 256;
+constexpr int kW4Stage = 512 * 128;
+// copy and barrier placement (measured: 8 / 8 / 32 beat 16 / -, 10 / 6, 6 / 8,
+// 4 / 6, 8 / 4 and 8 / 16 copies, and 24 or 40 MFMAs before the barrier)
+constexpr int kW4CopiesIn1b = 8;     // copies issued in (1b); the rest in (0)
+constexpr int kW4CopyGroups0 = 8;    // the first groups of (0) that carry them
+constexpr int kW4Mfma1a = 32;        // MFMAs of the second half before the barrier
 
-template <int BM, int BN, int WM, int WN, int NS, int BK, int EPI>
-__global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) {
-  typedef GemmCfg<BM, BN, WM, WN, NS, BK> C;
-  constexpr int CPR = BK / 8;  // 16-byte chunks per row
-  __shared__ __attribute__((aligned(1024))) char smem[NS * C::kStageBytes];
+template <int EPI>
+__global__ void __launch_bounds__(kW4Threads, 1) gemm_bf16_w4(GemmBf16Args p) {
+  constexpr int BM = 256, BN = 256, BK = 64;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * kW4Stage];
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid % kWave, l32 = lane & 31, hi = lane >> 5;
-  const int wm = wave / WN, wn = wave % WN;
+  const int wave = tid / kWave, lane = tid % kWave;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, lq = lane >> 4;
 
   // ---- tile id.  Unsplit launches take tiles [tile_base, tile_base +
   // gridDim.x) of the grouped order, remapped so that each XCD works through a
@@ -176,213 +180,172 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
   gemm_tile_of(pid, tm, tn, tile_m, tile_n);
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
-  // ---- copy plan: copy c of this wave fills kRowsPerCopy tile rows (1 KB) of
-  // A (rows < BM) or B; the lane lands in row kRowsPerCopy * idx + lane / CPR,
-  // slot lane % CPR.  The lane keeps a 32-bit byte offset into its matrix; the
-  // matrix base (advanced by one k-step per iteration) is wave-uniform.
-  uint32_t voff[C::kCopies];
-  bool is_a[C::kCopies];
-  uint32_t dst[C::kCopies];
-  const uint32_t lds0 = lds_offset(smem);
+  // ---- copy plan: copy c of this wave fills the 8 rows 8 (wave + 4 c) ..
+  // of the (A ++ B) stage, c < 8 in A; lane i takes row + i / 8, slot i % 8,
+  // which holds logical chunk (i % 8) ^ ((row >> 1) & 7)
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const bf16_t* b_base = n0 < p.n_split ? p.B0 : p.B1;  // BN divides n_split
   const int n_off = n0 < p.n_split ? n0 : n0 - p.n_split;
+  // The swizzled chunk of a lane, (lane % 8) ^ ((row >> 1) & 7), is the same
+  // for all its copies (rows 32 apart).  A rows may be gathered, so each A copy
+  // keeps its own offset; the B copies are one offset plus 32 rows per copy,
+  // folded into the wave-uniform base.
+  const int chunk = (lane % 8) ^ (((8 * wave_u + lane / 8) >> 1) & 7);
+  uint32_t voff_a[8];
 #pragma unroll
-  for (int c = 0; c < C::kCopies; ++c) {
-    const int idx = wave_u + C::kWaves * c;  // 1 KB block index within the stage
-    const int row = C::kRowsPerCopy * idx + lane / CPR;  // row of the (A ++ B) stage
-    const int chunk = gslot<BK>(row, lane % CPR);       // logical chunk in this lane's slot
-    is_a[c] = C::kRowsPerCopy * idx < BM;
-    if (is_a[c]) {
-      int m = m0 + row;
-      m = m < p.M ? m : p.M - 1;
-      const uint32_t ar = p.a_rows ? static_cast<uint32_t>(p.a_rows[m]) : static_cast<uint32_t>(m);
-      voff[c] = (ar * static_cast<uint32_t>(p.lda) + chunk * 8) * 2u;
-    } else {
-      const uint32_t n = n_off + row - BM;
-      voff[c] = (n * static_cast<uint32_t>(p.ldb) + chunk * 8) * 2u;
-    }
-    dst[c] = lds0 + idx * 1024;
+  for (int c = 0; c < 8; ++c) {
+    int m = m0 + 8 * (wave_u + 4 * c) + lane / 8;
+    m = m < p.M ? m : p.M - 1;
+    const uint32_t ar = p.a_rows ? static_cast<uint32_t>(p.a_rows[m]) : static_cast<uint32_t>(m);
+    voff_a[c] = (ar * static_cast<uint32_t>(p.lda) + chunk * 8) * 2u;
   }
-  auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
-    const bf16_t* sa = p.A + static_cast<int64_t>(kt) * BK;
-    const bf16_t* sb = b_base + static_cast<int64_t>(kt) * BK;
-#pragma unroll
-    for (int c = 0; c < C::kCopies; ++c)
-      lds_copy16_s(is_a[c] ? sa : sb, voff[c], dst[c] + stage * C::kStageBytes);
-  };
-  // refill source of the running k-step (set once per k-step)
-  const bf16_t* fill_a = p.A;
-  const bf16_t* fill_b = b_base;
-  uint32_t fill_off = 0;
-  auto issue_one = [&](int c) __attribute__((always_inline)) {
-    lds_copy16_s(is_a[c] ? fill_a : fill_b, voff[c], dst[c] + fill_off);
-  };
-
-  // ---- fragment read offsets (bytes within a stage): k16-step s reads chunk 2s + hi
-  constexpr int KS = BK / 16;  // k16-steps per k-step
-  int a_rd[KS], b_rd[KS];
-#pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    const int ra = wm * (BM / WM) + l32;  // + i * 32 rows: same swizzle, folded into the offset
-    const int rb = BM + wn * (BN / WN) + l32;
-    a_rd[s] = ra * C::kRowBytes + gslot<BK>(ra, 2 * s + hi) * 16;
-    b_rd[s] = rb * C::kRowBytes + gslot<BK>(rb, 2 * s + hi) * 16;
-  }
-
-  f32x16 acc[C::kTM][C::kTN];
-#pragma unroll
-  for (int i = 0; i < C::kTM; ++i)
-#pragma unroll
-    for (int j = 0; j < C::kTN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  // Fragments of two k16-steps live at once: step s+1 is read from LDS while
-  // the MFMAs of step s run.  sched_barrier pins that order (left alone, the
-  // scheduler hoists every read of a k-step above its MFMAs and runs out of
-  // registers).
-  bf16x8 fa[2][C::kTM], fb[2][C::kTN];
-  auto load = [&](auto set_c, int stage, int s) __attribute__((always_inline)) {
-    constexpr int SET = decltype(set_c)::value;
-    const char* base = smem + stage * C::kStageBytes;  // stage is wave-uniform, not unrolled
-#pragma unroll
-    for (int i = 0; i < C::kTM; ++i)
-      fa[SET][i] = *reinterpret_cast<const bf16x8*>(base + a_rd[s] + i * 32 * C::kRowBytes);
-#pragma unroll
-    for (int j = 0; j < C::kTN; ++j)
-      fb[SET][j] = *reinterpret_cast<const bf16x8*>(base + b_rd[s] + j * 32 * C::kRowBytes);
-  };
-  // MFMAs of one fragment set over accumulator rows [I0, I1), with the
-  // refill copies [Q0, Q1) spread evenly between them (group G of a k-step
-  // carries copies [G * kPerGroup, (G + 1) * kPerGroup)).
-  constexpr int kPerGroup = (C::kCopies + KS - 1) / KS;
-  auto mma = [&](auto set_c, auto i0_c, auto i1_c, auto g_c) __attribute__((always_inline)) {
-    constexpr int SET = decltype(set_c)::value;
-    constexpr int IA = decltype(i0_c)::value, IB = decltype(i1_c)::value, G = decltype(g_c)::value;
-    constexpr int NM = (IB - IA) * C::kTN;
-    constexpr int Q0 = G * kPerGroup < C::kCopies ? G * kPerGroup : C::kCopies;
-    constexpr int Q1 = Q0 + kPerGroup < C::kCopies ? Q0 + kPerGroup : C::kCopies;
-    constexpr int NQ = Q1 - Q0;
-#pragma unroll
-    for (int i = IA; i < IB; ++i)
-#pragma unroll
-      for (int j = 0; j < C::kTN; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[SET][i], fb[SET][j], acc[i][j], 0, 0, 0);
-        if constexpr (NQ > 0) {
-          const int t = (i - IA) * C::kTN + j;
-#pragma unroll
-          for (int q = 0; q < NQ; ++q)
-            if (t == q * NM / NQ) issue_one(Q0 + q);
-        }
-      }
-  };
-  typedef std::integral_constant<int, 0> I0;
-  typedef std::integral_constant<int, C::kTM / 2> IH;
-  typedef std::integral_constant<int, C::kTM> IM;
-  typedef std::integral_constant<int, (KS - 1) & 1> ILAST;
-
-  // NS-stage ring: k-step kt reads stage kt % NS while kt+1 .. kt+NS-1 are
-  // in flight.  The barrier of k-step kt sits inside its last MFMA group:
-  // before it, every wave has issued all its reads of stage kt % NS (which
-  // k-step kt+1 refills with kt+NS) and waited until at most its copies of
-  // the newest NS-2 k-steps are outstanding, so after it stage (kt+1) % NS is
-  // complete and its first fragments are read under the remaining MFMAs.
+  const uint32_t voff_b =
+      ((n_off + 8 * wave_u + lane / 8) * static_cast<uint32_t>(p.ldb) + chunk * 8) * 2u;
+  const int64_t b_copy_step = 32 * p.ldb;  // elements between consecutive B copies
+  const uint32_t dst0 = lds_offset(smem) + wave_u * 1024;  // copy c lands at dst0 + 4096 c
   const int nk_all = p.K / BK;
-  const int kt0 = split_k ? ksplit * p.kps : 0;  // first k-step of this workgroup
+  const int kt0 = split_k ? ksplit * p.kps : 0;
   const int nk = split_k ? (nk_all - kt0 < p.kps ? nk_all - kt0 : p.kps) : nk_all;  // >= 1
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
-    if (s < nk) issue(kt0 + s, s);
-  // Waits allow the copies of the NS-2 k-steps issued after the one needed;
-  // a range of fewer than NS-1 k-steps issued fewer, so it drains them all.
-  const bool short_range = nk < NS - 1;
-  auto wait_next = [&]() __attribute__((always_inline)) {
-    if (short_range)
-      __builtin_amdgcn_s_waitcnt(0);
-    else
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm((NS - 2) * C::kCopies));
+  const bf16_t* src_a = p.A;
+  const bf16_t* src_b = b_base;
+  uint32_t dst_stage = 0;
+  auto set_fill = [&](int kt, int stage) __attribute__((always_inline)) {
+    const int kf = kt0 + (kt < nk ? kt : nk - 1);
+    src_a = p.A + static_cast<int64_t>(kf) * BK;
+    src_b = b_base + static_cast<int64_t>(kf) * BK;
+    dst_stage = dst0 + stage * kW4Stage;
   };
-  wait_next();  // k-step 0 complete
+  auto copy = [&](auto c_c) __attribute__((always_inline)) {
+    constexpr int c = decltype(c_c)::value;
+    if constexpr (c < 8)
+      lds_copy16_s(src_a, voff_a[c], dst_stage + c * 4096);
+    else
+      lds_copy16_s(src_b + (c - 8) * b_copy_step, voff_b, dst_stage + c * 4096);
+  };
+
+  // ---- fragments: read q (0..15) of a k32 half is A block 0, then B blocks
+  // 0..7, then A blocks 1..7, the order the MFMAs (A block outer) use them
+  const int rd_a = (wm * 128 + l16) * 128, rd_b = (BM + wn * 128 + l16) * 128;
+  const int ch0 = (lq ^ (l16 >> 1)) * 16, ch1 = ((4 + lq) ^ (l16 >> 1)) * 16;
+  bf16x8 fa[2][8], fb[2][8];
+  auto read = [&](auto set_c, auto q_c, const char* base, int half) __attribute__((always_inline)) {
+    constexpr int SET = decltype(set_c)::value, Q = decltype(q_c)::value;
+    const int ch = half ? ch1 : ch0;
+    if constexpr (Q == 0)
+      fa[SET][0] = *reinterpret_cast<const bf16x8*>(base + rd_a + ch);
+    else if constexpr (Q <= 8)
+      fb[SET][Q - 1] = *reinterpret_cast<const bf16x8*>(base + rd_b + (Q - 1) * 2048 + ch);
+    else
+      fa[SET][Q - 8] = *reinterpret_cast<const bf16x8*>(base + rd_a + (Q - 8) * 2048 + ch);
+  };
+  f32x4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  auto mma = [&](auto set_c, auto t0_c, auto t1_c) __attribute__((always_inline)) {
+    constexpr int SET = decltype(set_c)::value, T0 = decltype(t0_c)::value, T1 = decltype(t1_c)::value;
+    static_for<T0, T1>([&](auto t_c) __attribute__((always_inline)) {
+      constexpr int T = decltype(t_c)::value;
+      acc[T / 8][T % 8] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[SET][T / 8], fb[SET][T % 8],
+                                                                  acc[T / 8][T % 8], 0, 0, 0);
+    });
+  };
+  typedef std::integral_constant<int, 0> S0;
+  typedef std::integral_constant<int, 1> S1;
+
+  // ---- prologue: k-steps 0 and 1 (or k-step 0 again) in flight, k-step 0
+  // complete; the MFMAs of k-step 0 up to the first barrier
+  set_fill(0, 0);
+  static_for<0, 16>(copy);
+  set_fill(1, 1);
+  static_for<0, 16>(copy);
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(16));
   __syncthreads();
-  load(I0{}, 0, 0);
-  int stage = 0;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int next = stage + 1 == NS ? 0 : stage + 1;
-    const int fill = stage == 0 ? NS - 1 : stage - 1;
-    // k-step kt + NS - 1 goes to the stage read at kt - 1; past the end the
-    // last k-step is fetched again (in bounds, never read) so that every
-    // k-step issues the same copies and the wait below is uniform.
-    const int kf = kt0 + (kt + NS - 1 < nk ? kt + NS - 1 : nk - 1);
-    fill_a = p.A + static_cast<int64_t>(kf) * BK;
-    fill_b = b_base + static_cast<int64_t>(kf) * BK;
-    fill_off = fill * C::kStageBytes;
-    static_for<0, KS - 1>([&](auto s_c) __attribute__((always_inline)) {
-      constexpr int S = decltype(s_c)::value;
+  static_for<0, 16>([&](auto q_c) __attribute__((always_inline)) { read(S0{}, q_c, smem, 0); });
+  // (0) of a k-step: the first half's 64 MFMAs with the second half's reads
+  // (and the copies that (1b) left, CS .. 15)
+  auto phase0 = [&](const char* stage, auto cs_c) __attribute__((always_inline)) {
+    constexpr int CS = decltype(cs_c)::value;
+    static_for<0, 16>([&](auto q_c) __attribute__((always_inline)) {
+      constexpr int Q = decltype(q_c)::value;
       __builtin_amdgcn_sched_barrier(0);
-      load(std::integral_constant<int, (S + 1) & 1>{}, stage, S + 1);
-      mma(std::integral_constant<int, S & 1>{}, I0{}, IM{}, s_c);
+      mma(S0{}, std::integral_constant<int, 4 * Q>{}, std::integral_constant<int, 4 * Q + 4>{});
+      read(S1{}, q_c, stage, 1);
+      // the copies CS .. 15 spread evenly over the first P0 groups
+      constexpr int NC = 16 - CS, P0 = kW4CopyGroups0;
+      if constexpr (Q < P0) static_for<CS + Q * NC / P0, CS + (Q + 1) * NC / P0>(copy);
     });
     __builtin_amdgcn_sched_barrier(0);
-    mma(ILAST{}, I0{}, IH{}, std::integral_constant<int, KS - 1>{});
-    __builtin_amdgcn_sched_barrier(0);
-    wait_next();  // k-step kt+1 complete
+  };
+  typedef std::integral_constant<int, 16> NoCopies;
+  constexpr int H1A = kW4Mfma1a;  // MFMAs of the second half before the barrier
+  typedef std::integral_constant<int, kW4CopiesIn1b> Cs;
+  phase0(smem, NoCopies{});
+  mma(S1{}, std::integral_constant<int, 0>{}, std::integral_constant<int, H1A>{});  // (1a)
+  __builtin_amdgcn_sched_barrier(0);
+  // One iteration: the barrier of k-step kt, its last 32 MFMAs (1b) with the
+  // first-half reads of kt + 1 and the first copies of kt + 2, then (0) and
+  // (1a) of kt + 1.  The reads of an iteration are used in that iteration.
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const char* nxt = smem + ((kt & 1) ^ 1) * kW4Stage;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // this wave's copies of k-step kt + 1
     __syncthreads();
-    if (kt + 1 < nk) load(I0{}, next, 0);
-    mma(ILAST{}, IH{}, IM{}, std::integral_constant<int, KS>{});
+    set_fill(kt + 2, kt & 1);
+    static_for<0, 16>([&](auto q_c) __attribute__((always_inline)) {
+      constexpr int Q = decltype(q_c)::value;
+      constexpr int M1 = 64 - H1A;  // MFMAs of (1b), spread over its 16 reads
+      __builtin_amdgcn_sched_barrier(0);
+      mma(S1{}, std::integral_constant<int, H1A + Q * M1 / 16>{},
+          std::integral_constant<int, H1A + (Q + 1) * M1 / 16>{});
+      read(S0{}, q_c, nxt, 0);
+      static_for<Q * Cs::value / 16, (Q + 1) * Cs::value / 16>(copy);
+    });
     __builtin_amdgcn_sched_barrier(0);
-    stage = next;
+    phase0(nxt, Cs{});
+    mma(S1{}, std::integral_constant<int, 0>{}, std::integral_constant<int, H1A>{});  // (1a)
+    __builtin_amdgcn_sched_barrier(0);
   }
-  __builtin_amdgcn_s_waitcnt(0);  // refetched k-steps still landing in LDS
+  mma(S1{}, std::integral_constant<int, H1A>{}, std::integral_constant<int, 64>{});  // (1b) of the last k-step
+  __builtin_amdgcn_s_waitcnt(0);  // re-fetched k-steps still landing in LDS
+  __syncthreads();
 
-  // ---- epilogue.  The 32x32 accumulator layout (lane holds column l32 and
-  // rows 8*(r/4) + 4*hi + r%4 of register r) is turned into row-contiguous
-  // pieces through LDS: each wave stages one 32-row slab of its tile at a
-  // time in a private region and reads it back as 4 consecutive columns per
-  // lane, so bias, gate and residual are read and the output written 8-16
-  // bytes per lane.  Staged rows are padded by 8 floats: the two half-waves
-  // (rows r and r+4) then write disjoint bank halves.
-  constexpr int WCOLS = C::kTN * 32;        // columns of a wave tile
-  constexpr int EP_LD = WCOLS + 8;          // staged row stride (floats)
-  constexpr int LPR = WCOLS / 4;            // lanes per staged row
-  constexpr int RPI = kWave / LPR;          // rows per read instruction
-  static_assert(C::kWaves * 32 * EP_LD * 4 <= NS * C::kStageBytes, "epilogue staging fits the ring");
-  __syncthreads();  // every wave is done with the ring
-  float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EP_LD;
-  const int c_l = (lane % LPR) * 4;                   // first of this lane's 4 columns
-  const int col = n0 + wn * (BN / WN) + c_l;           // global column (4 | col)
+  // ---- epilogue: each wave stages one 16-row group of its quarter at a time
+  // (lane holds column l16 and rows 4 lq .. 4 lq + 3 of every block) and reads
+  // it back as 4 consecutive columns per lane, two rows per read.  Rows are
+  // padded by 4 floats, so the four row groups of a write hit distinct banks.
+  constexpr int EP_LD = 128 + 4;
+  float* ep = reinterpret_cast<float*>(smem) + wave * 16 * EP_LD;
+  const int c_l = (lane % 32) * 4;
+  const int col = n0 + wn * 128 + c_l;
   float bias[4], gate[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (!split_k) gemm_col4<EPI>(p, col, bias, gate);
-  constexpr int NQ = 32 / RPI;                     // row groups of a slab per lane
-  constexpr int NR = EPI == EPI_GATE_RES ? NQ : 1;
+  constexpr int NR = EPI == EPI_GATE_RES ? 8 : 1;
 #pragma unroll
-  for (int i = 0; i < C::kTM; ++i) {
-    // the residuals of this lane's rows of the slab: every row index, then
-    // every residual, loaded together (rows past M load row M - 1, unused),
-    // in flight while the slab is staged
+  for (int i = 0; i < 8; ++i) {
     float res[NR][4];
     if constexpr (EPI == EPI_GATE_RES) {
       if (!split_k) {
-        int64_t rr[NQ];
+        int64_t rr[8];
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-          const int row = m0 + wm * (BM / WM) + i * 32 + q * RPI + lane / LPR;
+        for (int q = 0; q < 8; ++q) {
+          const int row = m0 + wm * 128 + i * 16 + 2 * q + lane / 32;
           rr[q] = row < p.M ? row : p.M - 1;
         }
         if (p.res_rows != nullptr) {
-          int g[NQ];
+          int g[8];
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) g[q] = p.res_rows[rr[q]];
+          for (int q = 0; q < 8; ++q) g[q] = p.res_rows[rr[q]];
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) rr[q] = g[q];
+          for (int q = 0; q < 8; ++q) rr[q] = g[q];
         }
         if (p.res_bf16) {
           const bf16_t* rb = static_cast<const bf16_t*>(p.res) + col;
-          uint2 raw[NQ];
+          uint2 raw[8];
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) raw[q] = ldg8_nt(rb + rr[q] * p.ldr);
+          for (int q = 0; q < 8; ++q) raw[q] = ldg8_nt(rb + rr[q] * p.ldr);
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) {
+          for (int q = 0; q < 8; ++q) {
             res[q][0] = __uint_as_float(raw[q].x << 16);
             res[q][1] = __uint_as_float(raw[q].x & 0xffff0000u);
             res[q][2] = __uint_as_float(raw[q].y << 16);
@@ -390,11 +353,11 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
           }
         } else {
           const float* rf = static_cast<const float*>(p.res) + col;
-          uint4 raw[NQ];
+          uint4 raw[8];
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) raw[q] = ldg16_nt(rf + rr[q] * p.ldr);
+          for (int q = 0; q < 8; ++q) raw[q] = ldg16_nt(rf + rr[q] * p.ldr);
 #pragma unroll
-          for (int q = 0; q < NQ; ++q) {
+          for (int q = 0; q < 8; ++q) {
             res[q][0] = __uint_as_float(raw[q].x);
             res[q][1] = __uint_as_float(raw[q].y);
             res[q][2] = __uint_as_float(raw[q].z);
@@ -404,18 +367,16 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_bf16_nt(GemmBf16Args p) 
       }
     }
 #pragma unroll
-    for (int j = 0; j < C::kTN; ++j)
+    for (int j = 0; j < 8; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        ep[(8 * (r >> 2) + 4 * hi + (r & 3)) * EP_LD + j * 32 + l32] = acc[i][j][r];
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(63));  // this wave's staged slab is in LDS (LDS only)
+      for (int r = 0; r < 4; ++r) ep[(4 * lq + r) * EP_LD + j * 16 + l16] = acc[i][j][r];
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(63));  // this wave's staged group is in LDS
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int r_l = q * RPI + lane / LPR;
-      const int trow = wm * (BM / WM) + i * 32 + r_l;  // row within the tile
+    for (int q = 0; q < 8; ++q) {
+      const int r_l = 2 * q + lane / 32;
+      const int trow = wm * 128 + i * 16 + r_l;
       const float4 a4 = *reinterpret_cast<const float4*>(ep + r_l * EP_LD + c_l);
       if (split_k) {
-        // raw partial sums of this k-range, tile-local [BM][BN] per workgroup
         *reinterpret_cast<float4*>(p.part + static_cast<int64_t>(blockIdx.x) * BM * BN +
                                    static_cast<int64_t>(trow) * BN + (col - n0)) = a4;
       } else if (m0 + trow < p.M) {
@@ -454,9 +415,17 @@ __global__ void __launch_bounds__(256) gemm_splitk_reduce(GemmBf16Args p, int nt
   gemm_store4<EPI>(p, row, tile_n * BN + 4 * c4, v, bias, gate, res);
 }
 
-template <int BM, int BN, int WM, int WN, int NS, int BK, int EPI>
+// The tile kernel the launcher runs.
+template <int EPI>
+struct GemmW4 {
+  static constexpr int kThreads = kW4Threads;
+  static void launch(int grid, const GemmBf16Args& a, hipStream_t stream) {
+    hipLaunchKernelGGL((gemm_bf16_w4<EPI>), dim3(grid), dim3(kThreads), 0, stream, a);
+  }
+};
+
+template <int BM, int BN, int BK, int EPI, typename KERNEL>
 hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream) {
-  typedef GemmCfg<BM, BN, WM, WN, NS, BK> C;
   const int tiles = ((a.M + BM - 1) / BM) * (a.N / BN);
   const int nk = a.K / BK;
   // Tiles beyond the last full round (one workgroup per CU) are split along
@@ -468,7 +437,7 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   // Each split also writes and the reduce reads a 256 KB fp32 partial tile:
   // below about 20 k-steps per split that costs more than the shorter range
   // saves (160 k-steps: 8 splits beat 16 by 7-11 us; 432: 16 beat 8).
-  constexpr int kMinStepsPerSplit = 20;
+  constexpr int kMinStepsPerSplit = 640 / BK;
   const int cap = nk / kMinStepsPerSplit > 1 ? nk / kMinStepsPerSplit : 1;
   nsplit = nsplit < cap ? nsplit : cap;
   const size_t unit_bytes = sizeof(float) * BM * BN;
@@ -478,7 +447,7 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   a.tile_base = 0;
   if (nsplit < 2) {
     a.nsplit = 1;
-    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI>), dim3(tiles), dim3(C::kThreads), 0, stream, a);
+    KERNEL::launch(tiles, a, stream);
     return hipGetLastError();
   }
   a.kps = (nk + nsplit - 1) / nsplit;  // k-steps per split
@@ -486,14 +455,13 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   const int full = tiles - tail;
   if (full > 0) {
     a.nsplit = 1;
-    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI>), dim3(full), dim3(C::kThreads), 0, stream, a);
+    KERNEL::launch(full, a, stream);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   a.tile_base = full;
   a.nsplit = nsplit;
-  hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, NS, BK, EPI>), dim3(tail * nsplit), dim3(C::kThreads), 0,
-                     stream, a);
+  KERNEL::launch(tail * nsplit, a, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t threads = static_cast<int64_t>(tail) * BM * (BN / 4);
@@ -502,14 +470,14 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int NS, int BK>
-hipError_t launch_gemm_tile(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream) {
+hipError_t launch_gemm_w4(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream) {
+  constexpr int BM = 256, BN = 256, BK = 64;
   if (a.N % BN != 0 || (a.n_split < a.N && a.n_split % BN != 0) || a.K % BK != 0)
     return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_BIAS: return launch_gemm_epi<BM, BN, WM, WN, NS, BK, EPI_BIAS>(name, a, stream);
-    case EPI_GELU: return launch_gemm_epi<BM, BN, WM, WN, NS, BK, EPI_GELU>(name, a, stream);
-    default: return launch_gemm_epi<BM, BN, WM, WN, NS, BK, EPI_GATE_RES>(name, a, stream);
+    case EPI_BIAS: return launch_gemm_epi<BM, BN, BK, EPI_BIAS, GemmW4<EPI_BIAS>>(name, a, stream);
+    case EPI_GELU: return launch_gemm_epi<BM, BN, BK, EPI_GELU, GemmW4<EPI_GELU>>(name, a, stream);
+    default: return launch_gemm_epi<BM, BN, BK, EPI_GATE_RES, GemmW4<EPI_GATE_RES>>(name, a, stream);
   }
 }
 
@@ -519,7 +487,7 @@ hipError_t launch_gemm_bf16(const char* name, int epi, const GemmBf16Args& a, hi
   const int64_t lim = int64_t(1) << 31;
   if (a.a_nrows <= 0 || a.a_nrows * a.lda * 2 >= lim || int64_t(a.N) * a.ldb * 2 >= lim)
     return hipErrorInvalidValue;
-  return launch_gemm_tile<256, 256, 2, 4, 4, 32>(name, epi, a, stream);
+  return launch_gemm_w4(name, epi, a, stream);
 }
 
 }  // namespace echo

@@ -12,6 +12,11 @@ with its default output format).
         counters of a copy of known size (the hbm_copy module: 1 GiB read and
         1 GiB written), as JSON records keyed KEY carrying the sha256 of SOURCE
         (the kernel's source file, so that a stale record can be recognised)
+    python -m paper_2608_02474_amd.rocpd_summary mfma PATTERN RUN.db [RUN.db ...]
+        per (kernel, grid size) matching PATTERN: shader clock, MFMA-busy
+        fraction, MFMA work issued, vector instructions per MFMA, wait and LDS
+        bank-conflict fractions from counter runs (each with --kernel-trace
+        for the durations), then every raw counter average
 
 Grouping by grid size separates dispatches of one kernel at different
 problem sizes (for example the all-token first step from the cached steps).
@@ -87,6 +92,72 @@ def traffic(fetch_db, write_db, copy_fetch_db, copy_write_db, specs):
     return out
 
 
+def dispatch_durations(db: str):
+    """{(kernel, grid threads): average duration in ns} from the kernel trace
+    of a run (empty if the run recorded none)."""
+    c = sqlite3.connect(db)
+    try:
+        q = ("select name, grid_x * grid_y * grid_z, avg(duration) from kernels "
+             "group by name, grid_x, grid_y, grid_z")
+        return {(short_name(r[0]), r[1]): r[2] for r in c.execute(q)}
+    except sqlite3.Error:
+        return {}
+
+
+def counter_table(dbs, pattern: str = ""):
+    """Average value per dispatch of every counter in the given runs, per
+    (kernel, grid threads) whose name contains `pattern`, with the average
+    dispatch duration: {(kernel, grid): {"calls": n, "dur_ns": t, COUNTER: v}}."""
+    out = {}
+    for db in dbs:
+        dur = dispatch_durations(db)
+        c = sqlite3.connect(db)
+        q = ("select kernel_name, grid_size, counter_name, count(*), avg(value) from counters_collection "
+             "where kernel_name like ? group by kernel_name, grid_size, counter_name")
+        for name, grid, counter, n, v in c.execute(q, (f"%{pattern}%",)):
+            key = (short_name(name), grid)
+            rec = out.setdefault(key, {"calls": n})
+            rec[counter] = float(v)
+            if key in dur:
+                rec.setdefault("dur_ns", dur[key])
+    return out
+
+
+def mfma_summary(dbs, pattern: str = "", simds: int = 1024, xcds: int = 8):
+    """Per-dispatch MFMA evidence of the kernels matching `pattern`.
+    GRBM_GUI_ACTIVE is summed over the 8 XCDs (each counts its own busy
+    cycles), SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs:
+      sclk        GRBM_GUI_ACTIVE / 8 / duration (GHz), the shader clock while it ran
+      mfma_busy   SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024 SIMDs):
+                  the fraction of the SIMDs' cycles their MFMA pipe was busy
+      peak_frac   mfma_busy x sclk / 2.4 GHz: the same against the nominal clock
+      bf16_tflop  SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (the MFMA work issued)
+      valu/mfma   SQ_INSTS_VALU / SQ_INSTS_MFMA (vector instructions per MFMA)
+      coexec      SQ_VALU_MFMA_COEXEC_CYCLES / SQ_VALU_MFMA_BUSY_CYCLES
+      wait        SQ_WAIT_ANY / SQ_WAVE_CYCLES and SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES
+      lds_bank    SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE"""
+    rows = []
+    for (name, grid), r in sorted(counter_table(dbs, pattern).items(), key=lambda kv: -kv[1].get("dur_ns", 0)):
+        g = r.get("GRBM_GUI_ACTIVE")
+        d = r.get("dur_ns")
+        busy = r.get("SQ_VALU_MFMA_BUSY_CYCLES")
+        ratio = lambda a, b: (r[a] / r[b]) if r.get(a) is not None and r.get(b) else None
+        sclk = g / xcds / d if g and d else None
+        mb = busy / (g / xcds * simds) if busy is not None and g else None
+        rows.append({"kernel": name, "grid": grid, "calls": r["calls"], "dur_us": d / 1e3 if d else None,
+                     "sclk_ghz": sclk, "mfma_busy": mb,
+                     "peak_frac": mb * sclk / 2.4 if mb is not None and sclk else None,
+                     "bf16_tflop": r["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 / 1e12
+                     if r.get("SQ_INSTS_VALU_MFMA_MOPS_BF16") is not None else None,
+                     "valu_per_mfma": ratio("SQ_INSTS_VALU", "SQ_INSTS_MFMA"),
+                     "coexec": ratio("SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES"),
+                     "wait_any": ratio("SQ_WAIT_ANY", "SQ_WAVE_CYCLES"),
+                     "wait_inst": ratio("SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES"),
+                     "lds_bank": ratio("SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE"),
+                     "raw": {k: v for k, v in r.items() if k not in ("calls", "dur_ns")}})
+    return rows
+
+
 def main(argv):
     if len(argv) >= 2 and argv[0] == "trace":
         print(f"{'kernel':58s} {'grid threads':>12s} {'calls':>5s} {'avg us':>10s} "
@@ -98,6 +169,20 @@ def main(argv):
         print(f"{'kernel':58s} {'grid threads':>12s} {'calls':>5s} {argv[2] + ' (KiB)':>16s}")
         for n, g, k, v in counter_rows(argv[1], argv[2]):
             print(f"{n[:58]:58s} {g:12d} {k:5d} {v:16.1f}")
+        return 0
+    if len(argv) >= 3 and argv[0] == "mfma":
+        pattern, dbs = argv[1], argv[2:]
+        cols = ("dur_us", "sclk_ghz", "mfma_busy", "peak_frac", "bf16_tflop", "valu_per_mfma", "coexec",
+                "wait_any", "wait_inst", "lds_bank")
+        print(f"{'kernel':44s} {'grid':>9s} " + " ".join(f"{c:>13s}" for c in cols))
+        rows = mfma_summary(dbs, pattern)
+        for r in rows:
+            vals = " ".join(f"{r[c]:13.4f}" if r[c] is not None else f"{'-':>13s}" for c in cols)
+            print(f"{r['kernel'][:44]:44s} {r['grid']:9d} {vals}")
+        print("\nraw counters per dispatch (averages):")
+        for r in rows:
+            print(f"{r['kernel'][:44]:44s} {r['grid']:9d} " +
+                  " ".join(f"{k}={v:.6g}" for k, v in sorted(r["raw"].items())))
         return 0
     if len(argv) >= 6 and argv[0] == "traffic":
         print(json.dumps(traffic(*argv[1:5], argv[5:]), indent=1))
