@@ -19,19 +19,24 @@
 //   * K and V^T fragments flow through a small register ring, each read
 //     issued a fixed number of MFMAs ahead of its use.
 //   * softmax per lane: a lane owns one query per block (its accumulator
-//     column) and half of the tile's keys; the row max uses one
-//     v_permlane32_swap.  The scale is folded into one FMA before exp2;
-//     masking runs only on the ragged last tile; a row's running output is
-//     rescaled only when the tile raises its maximum by more than 2^8 (rows
-//     that keep their maximum are untouched, so each row's arithmetic depends
-//     on its own scores only).
+//     column) and half of the tile's keys.  The exp2 argument s c - m c (c =
+//     scale log2 e) is one FMA against a per-row reference m c, which is
+//     the first half's row maximum and moves only when a half's largest
+//     argument exceeds 8 (lazy rescale, by that argument).  No per-tile row
+//     maximum is taken: a probability above 2^8 implies a lane sum above
+//     2^8, so the common case costs one compare on the row sum; the wave
+//     enters the exact path (row maxima, shift, recomputed probabilities)
+//     only then, and rows that do not grow get a zero shift and the same
+//     values, so each row's arithmetic depends on its own scores only.
+//     Masking runs only on the ragged last tile.
 //   * O^T (dh x queries) += V^T . P^T: P^T is the S accumulator converted to
 //     bf16 in registers; V^T fragments come straight from the row-major V tile
 //     with ds_read_b64_tr_b16 (LDS transpose reads), two per 8-key operand.
-//   * The key loop is software-pipelined by one tile: the exp / pack / row
-//     sum of tile t is spread between the MFMAs of S(t+1), and the row maximum
-//     of S(t+1) between the MFMAs of PV(t), so each wave's vector work runs
-//     under its own matrix work (two accumulator sets for S).
+//   * The key loop is software-pipelined by one half (32 keys): the exp /
+//     pack / row sum of half h run between the S MFMAs of half h + 1, and
+//     the exp2 arguments of half h + 1 with its first chunks between the PV
+//     MFMAs of half h, so that neither phase has much more vector work than
+//     matrix work (two accumulator sets for S).
 //   * In the steady state a wave's copies of a new tile are issued one at a
 //     time between the S MFMAs after the tile barrier, not all at once at the
 //     barrier: eight waves issuing their copies together made each wait at
@@ -57,6 +62,9 @@ constexpr int ATT_NSTAGE = 4;                         // K/V ring stages
 constexpr int ATT_V_BASE = ATT_NSTAGE * ATT_TILE_BYTES;  // 64 KB
 constexpr int ATT_OS_STRIDE = ATT_DH + 8;            // output staging row (bf16)
 constexpr float ATT_RESCALE_LOG2 = 8.0f;             // lazy-rescale headroom (log2 units)
+constexpr float ATT_RESCALE_SUM = 256.0f;            // 2^ATT_RESCALE_LOG2
+constexpr int ATT_NPRE = 3;     // chunks of a half's softmax done under the PV MFMAs before it
+constexpr int ATT_PV_EXP0 = 2;  // PV MFMA after which the first of those chunks takes its exp2
 constexpr int ATT_RING = 2;                          // LDS fragment reads in flight per wave
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -267,12 +275,11 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[b][d][r] = 0.0f;
-  float m_run[QB], l_run[QB];
+  // mc: the row's reference maximum times scale_log2 (exp2 units); l_run:
+  // running sum of the probabilities, relative to the same reference
+  float mc[QB], l_run[QB];
 #pragma unroll
-  for (int b = 0; b < QB; ++b) {
-    m_run[b] = -INFINITY;
-    l_run[b] = 0.0f;
-  }
+  for (int b = 0; b < QB; ++b) l_run[b] = 0.0f;
 
   const f32x16 zero16 = {};
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
@@ -341,67 +348,27 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       for (int b = 0; b < QB; ++b) sh[b][r] = valid ? sh[b][r] : -INFINITY;
     }
   };
-  // running maximum of elements 2c, 2c + 1 (chunk c of 8)
-  auto max_chunk = [&](const f32x16(&sh)[QB], int c, float(&m)[QB]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < QB; ++b) m[b] = fmaxf(fmaxf(m[b], sh[b][2 * c]), sh[b][2 * c + 1]);
-  };
-  // lazy rescale: only rows whose maximum grows by more than 2^8 move their
-  // reference; the others keep it (alpha = 1, untouched)
-  auto update_max = [&](const float(&m)[QB]) __attribute__((always_inline)) {
+  // Softmax of a half in chunks of two scores (chunk c: elements 2c, 2c + 1,
+  // probabilities pf[b][c / 4][2 (c % 4) ..]).  Three steps, placed apart:
+  // the exp2 argument s scale_log2 - mc, in place; its exp2; the bf16 pack
+  // (the PV operand) and the row sum of the same bf16 values, two per v_dot2.
+  auto arg_chunk = [&](f32x16(&sh)[QB], int c) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      const float mx = pair_max(m[b]);
-      const bool grow = (mx - m_run[b]) * scale_log2 > ATT_RESCALE_LOG2;
-      if (__builtin_expect(__ballot(grow) != 0ull, 0)) {
-        const float m_new = grow ? mx : m_run[b];
-        const float alpha = grow ? __builtin_amdgcn_exp2f((m_run[b] - m_new) * scale_log2) : 1.0f;
-        m_run[b] = m_new;
-        l_run[b] *= alpha;
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[b][d][r] *= alpha;
-      }
+      sh[b][2 * c] = fmaf(sh[b][2 * c], scale_log2, -mc[b]);
+      sh[b][2 * c + 1] = fmaf(sh[b][2 * c + 1], scale_log2, -mc[b]);
     }
   };
-  // probabilities of elements 8a + j, 8a + j + 1 (chunk c of 8: a = c / 4,
-  // j = 2 (c % 4)): exp2 of the scaled, shifted scores, packed to bf16 (the
-  // PV operand), and the row sum of the same bf16 values, two per v_dot2
-  auto exp_chunk = [&](const f32x16(&sh)[QB], int c, const float(&neg_mc)[QB], float(&psum)[QB],
-                       bf16x8(&pf)[QB][2]) __attribute__((always_inline)) {
-    const int a = c / 4, j = 2 * (c % 4);
+  auto exp_chunk = [&](const f32x16(&sh)[QB], int c, float(&t)[QB][2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      pf[b][a][j] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sh[b][8 * a + j], scale_log2, neg_mc[b])));
-      pf[b][a][j + 1] =
-          static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sh[b][8 * a + j + 1], scale_log2, neg_mc[b])));
-      const bf16x2 pair = {pf[b][a][j], pf[b][a][j + 1]};
-      psum[b] = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, psum[b], false);
+      t[b][0] = __builtin_amdgcn_exp2f(sh[b][2 * c]);
+      t[b][1] = __builtin_amdgcn_exp2f(sh[b][2 * c + 1]);
     }
   };
-  // The same three steps split for software pipelining across chunks, so
-  // that the vector work placed after one MFMA has no dependence inside it:
-  // the scaled, shifted scores of chunk c; their exp2; the bf16 pack and row
-  // sum (same operations and order as exp_chunk).
-  auto exp_arg = [&](const f32x16(&sh)[QB], int c, const float(&neg_mc)[QB], float(&t)[QB][2])
-      __attribute__((always_inline)) {
-    const int a = c / 4, j = 2 * (c % 4);
-#pragma unroll
-    for (int b = 0; b < QB; ++b) {
-      t[b][0] = fmaf(sh[b][8 * a + j], scale_log2, neg_mc[b]);
-      t[b][1] = fmaf(sh[b][8 * a + j + 1], scale_log2, neg_mc[b]);
-    }
-  };
-  auto exp_val = [&](float(&t)[QB][2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < QB; ++b) {
-      t[b][0] = __builtin_amdgcn_exp2f(t[b][0]);
-      t[b][1] = __builtin_amdgcn_exp2f(t[b][1]);
-    }
-  };
-  auto exp_pack = [&](int c, const float(&t)[QB][2], float(&psum)[QB], bf16x8(&pf)[QB][2])
-      __attribute__((always_inline)) {
+  bf16x8 pf[QB][2];
+  float psum[QB];
+  auto pack_chunk = [&](int c, const float(&t)[QB][2]) __attribute__((always_inline)) {
     const int a = c / 4, j = 2 * (c % 4);
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
@@ -411,31 +378,91 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       psum[b] = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, psum[b], false);
     }
   };
-  auto exp_begin = [&](float(&neg_mc)[QB], float(&psum)[QB]) __attribute__((always_inline)) {
+  // Lazy rescale.  The arguments are taken against the reference mc; a row
+  // moves its reference only when the half's largest argument exceeds
+  // ATT_RESCALE_LOG2 (its maximum grew by more than 2^8), by that argument.
+  // No probability can exceed 2^8 unless the lane's sum does, so the common
+  // case costs one compare on the sum; the wave enters the exact path only
+  // when some lane's sum is above 2^8.  There, rows that do not grow get a
+  // shift of 0 and recompute the same values: each row's arithmetic depends
+  // on its own scores only.
+  auto settle_exact = [&](f32x16(&sh)[QB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      neg_mc[b] = -m_run[b] * scale_log2;
+      float mx = sh[b][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sh[b][r]);
+      mx = pair_max(mx);
+      const float d = mx > ATT_RESCALE_LOG2 ? mx : 0.0f;
+      const float alpha = __builtin_amdgcn_exp2f(-d);
+      mc[b] += d;
+      l_run[b] *= alpha;
+#pragma unroll
+      for (int dd = 0; dd < 4; ++dd)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[b][dd][r] *= alpha;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sh[b][r] -= d;
       psum[b] = 0.0f;
     }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      float t[QB][2];
+      exp_chunk(sh, c, t);
+      pack_chunk(c, t);
+    }
   };
-  auto exp_end = [&](const float(&psum)[QB]) __attribute__((always_inline)) {
+  auto any_big = [&]() __attribute__((always_inline)) {
+    bool big = false;
+#pragma unroll
+    for (int b = 0; b < QB; ++b) big = big || psum[b] > ATT_RESCALE_SUM;
+    return __ballot(big) != 0ull;
+  };
+  auto add_sum = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < QB; ++b) l_run[b] += psum[b];
   };
+  // A half's softmax starts (arguments of all chunks, probabilities of chunks
+  // 0 .. ATT_NPRE - 1) under the PV MFMAs of the half before it and finishes
+  // under the S MFMAs of the half after it.
+  constexpr int NPRE = ATT_NPRE, NJ = 8 - NPRE;
+  auto begin_half = [&](f32x16(&sh)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) arg_chunk(sh, c);
+#pragma unroll
+    for (int b = 0; b < QB; ++b) psum[b] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NPRE; ++c) {
+      float t[QB][2];
+      exp_chunk(sh, c, t);
+      pack_chunk(c, t);
+    }
+  };
+  auto finish_half = [&](f32x16(&sh)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = NPRE; c < 8; ++c) {
+      float t[QB][2];
+      exp_chunk(sh, c, t);
+      pack_chunk(c, t);
+    }
+    if (__builtin_expect(any_big(), 0)) settle_exact(sh);
+    add_sum();
+  };
 
   // ---- the key loop, software-pipelined by one half.  Half h starts with
-  // S_h in one accumulator set, its maximum already applied:
+  // the arguments of S_h in one accumulator set and its first NPRE chunks
+  // packed:
   //   at a tile boundary (h + 1 even): wait for tile (h + 1) / 2; barrier
   //     (every wave is past the PV of tile (h + 1) / 2 - 2, whose stage is
   //     free); issue tile (h + 1) / 2 + 2;
-  //   A: the 8 MFMAs of S_{h+1}  +  exp / pack / row sum of half h
-  //   B: the 8 MFMAs of PV_h     +  row maximum of S_{h+1};  lazy rescale.
+  //   A: the 8 MFMAs of S_{h+1}  +  exp / pack / row sum of the rest of half h;
+  //      settle half h (lazy rescale, row sum);
+  //   B: the 8 MFMAs of PV_h     +  arguments of S_{h+1}, its first chunks.
   // Each wave's vector work thus runs under its own matrix work.  The
   // steady state runs in blocks of 8 halves (4 tiles, one turn of the stage
-  // ring) whose halves have no key past L, as straight-line code (a branch
-  // between the phases would let the compiler move the vector work out of
-  // the MFMA sequence); the remaining halves, the ragged one included, take a
-  // plain per-half path.  Tiles are counted from t_begin.
+  // ring) whose halves have no key past L, as straight-line code; the
+  // remaining halves, the ragged one included, take a plain per-half path.
+  // Tiles are counted from t_begin.
   const int key_begin = t_begin * ATT_KT;
   const int nh = 2 * nkt;
   const int nh_full = (L - key_begin) / 32 < nh ? (L - key_begin) / 32 : nh;  // halves with no key past L
@@ -445,10 +472,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     __syncthreads();
     issue_tile(t + 2, stage_next2);
   };
-  auto fresh_max = [&](float(&m)[QB]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < QB; ++b) m[b] = -INFINITY;
-  };
   f32x16 s0[QB], s1[QB];
   issue_tile(0, 0);
   issue_tile(1, 1);
@@ -456,11 +479,16 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   {
     s_half(smem, 0, s0, [](int) {});
     if (key_begin + 32 > L) mask_half(s0, key_begin);
-    float m[QB];
-    fresh_max(m);
+    // the first reference: the row maximum of the first half (every row has
+    // a key there)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) max_chunk(s0, c, m);
-    update_max(m);
+    for (int b = 0; b < QB; ++b) {
+      float mx = s0[b][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s0[b][r]);
+      mc[b] = pair_max(mx) * scale_log2;
+    }
+    begin_half(s0);
   }
 
   // H = h % 8: tile h / 2 in stage H / 2, key block H % 2, S_h in set H % 2
@@ -470,9 +498,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     constexpr int HN = (H + 1) % 8, STN = HN / 2, KBN = HN % 2;
     auto& sc = pick2<KB>(s0, s1);
     auto& sn = pick2<1 - KB>(s0, s1);
-    bf16x8 pf[QB][2];
-    float neg_mc[QB], psum[QB], m[QB];
-    exp_begin(neg_mc, psum);
     if constexpr (KBN == 0) {
       // this wave's copies of the new tile have landed; after the barrier
       // every wave is past the tile whose stage the copies below refill
@@ -480,31 +505,50 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       __syncthreads();
       tile_prep((h + 1) / 2 + 2, (STN + 2) % ATT_NSTAGE);
     }
-    // chunk c: arguments after S MFMA c, exp2 after MFMA c + 1, pack and
-    // row sum after MFMA c + 2; chunk 7's exp2 and the packs of chunks 6
-    // and 7 go under the first PV MFMAs (which read keys 0-15 only)
-    float tq[3][QB][2];
+    // chunk NPRE + j: exp2 after S MFMA 8 j / NJ, pack and row sum after the next
+    float tq[2][QB][2];
     s_half(smem + STN * ATT_TILE_BYTES, KBN, sn, [&](int i) __attribute__((always_inline)) {
-      exp_arg(sc, i, neg_mc, tq[i % 3]);
-      if (i >= 1) exp_val(tq[(i + 2) % 3]);
-      if (i >= 2) exp_pack(i - 2, tq[(i + 1) % 3], psum, pf);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if (i == (8 * j) / NJ) exp_chunk(sc, NPRE + j, tq[j % 2]);
+        if (i == (8 * j) / NJ + 1) pack_chunk(NPRE + j, tq[j % 2]);
+      }
       if constexpr (KBN == 0) {
         // the wave's NC copies of the tile, spread evenly over the 8 MFMAs
 #pragma unroll
         for (int c = (i * NC) / 8; c < ((i + 1) * NC) / 8; ++c) tile_copy(c);
       }
     });
-    fresh_max(m);
+    // the arguments of S_h are gone (their registers were reused as the
+    // chunks finished); the exact path recomputes S_h from the K tile, still
+    // in its stage, by the same MFMA sequence (the same values)
+    if (__builtin_expect(any_big(), 0)) {
+      f32x16 sr[QB];
+      s_half(smem + ST * ATT_TILE_BYTES, KB, sr, [](int) {});
+#pragma unroll
+      for (int c = 0; c < 8; ++c) arg_chunk(sr, c);
+      settle_exact(sr);
+    }
+    add_sum();
+#pragma unroll
+    for (int b = 0; b < QB; ++b) psum[b] = 0.0f;
+    // S_{h+1}: arguments of chunks 0 .. NPRE - 1 after PV MFMA 0, their exp2
+    // after MFMAs 2 .., each pack one MFMA later (the first four PV MFMAs read
+    // the packed keys 0-15); the other arguments after MFMAs 4-7
     pv_half(smem + ST * ATT_TILE_BYTES, KB, pf, [&](int i) __attribute__((always_inline)) {
       if (i == 0) {
-        exp_val(tq[7 % 3]);
-        exp_pack(6, tq[6 % 3], psum, pf);
+#pragma unroll
+        for (int c = 0; c < NPRE; ++c) arg_chunk(sn, c);
       }
-      if (i == 1) exp_pack(7, tq[7 % 3], psum, pf);
-      max_chunk(sn, i, m);
+#pragma unroll
+      for (int c = 0; c < NPRE; ++c) {
+        if (i == ATT_PV_EXP0 + c) exp_chunk(sn, c, tq[c % 2]);
+        if (i == ATT_PV_EXP0 + 1 + c) pack_chunk(c, tq[c % 2]);
+      }
+#pragma unroll
+      for (int k = 0; k < NJ; ++k)
+        if (i == 4 + (4 * k) / NJ) arg_chunk(sn, NPRE + k);
     });
-    exp_end(psum);
-    update_max(m);
   };
   int h = 0;
   for (; h + 8 < nh_full; h += 8) {
@@ -519,12 +563,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
   // The remaining halves one at a time (S_h is in s0, tile h / 2 in stage 0).
   for (; h < nh; ++h) {
-    bf16x8 pf[QB][2];
-    float neg_mc[QB], psum[QB];
-    exp_begin(neg_mc, psum);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) exp_chunk(s0, c, neg_mc, psum, pf);
-    exp_end(psum);
+    finish_half(s0);
     pv_half(smem + ((h / 2) % ATT_NSTAGE) * ATT_TILE_BYTES, h % 2, pf, [](int) {});
     if (h + 1 < nh) {
       const int hn = h + 1, stn = (hn / 2) % ATT_NSTAGE;
@@ -532,11 +571,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
       s_half(smem + stn * ATT_TILE_BYTES, hn % 2, s0, [](int) {});
       const int keyh = key_begin + hn * 32;
       if (keyh + 32 > L) mask_half(s0, keyh);
-      float m[QB];
-      fresh_max(m);
-#pragma unroll
-      for (int c = 0; c < 8; ++c) max_chunk(s0, c, m);
-      update_max(m);
+      begin_half(s0);
     }
   }
   // drain the copies still in flight (re-copies past the last tile) before
@@ -545,15 +580,15 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
 
   if (part_o != nullptr) {
     // split workgroup: unnormalised output in the accumulator layout (for each
-    // (b, d, r) the 64 lanes write 256 contiguous bytes), running reference
-    // maximum and row sum per query
+    // (b, d, r) the 64 lanes write 256 contiguous bytes), reference maximum
+    // (exp2 units) and row sum per query
     const int64_t unit = blockIdx.x;
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
       const float lsum = pair_sum(l_run[b]);
       const int qloc = (wave * QB + b) * 32 + l32;
       if (hi == 0) {
-        part_ml[(unit * C::kQ + qloc) * 2] = m_run[b];
+        part_ml[(unit * C::kQ + qloc) * 2] = mc[b];
         part_ml[(unit * C::kQ + qloc) * 2 + 1] = lsum;
       }
       float* po = part_o + ((unit * WAVES + wave) * QB + b) * (4 * 16 * kWave);
@@ -592,9 +627,9 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
   }
 }
 
-// Merge the key-range splits of the tail items: o = sum_s 2^{(m_s - m) c} o_s
-// / sum_s 2^{(m_s - m) c} l_s with m = max_s m_s (c = scale * log2 e), splits
-// added in order.  One workgroup per 32-query block of an item: its threads
+// Merge the key-range splits of the tail items: o = sum_s 2^{r_s - r} o_s /
+// sum_s 2^{r_s - r} l_s, where r_s is split s's reference maximum in exp2
+// units (times scale log2 e) and r = max_s r_s, splits added in order.  One workgroup per 32-query block of an item: its threads
 // take the block's 4096 outputs in the order the partials are stored (the
 // accumulator layout: lane fastest), so every split's partial is read with
 // consecutive addresses, and the bf16 results go through LDS so that the
@@ -636,7 +671,7 @@ attn_combine(const float* __restrict__ part_o, const float* __restrict__ part_ml
     float lsum = 0.0f, acc = 0.0f;
     for (int sp = 0; sp < nsplit; ++sp) {
       const int64_t unit = static_cast<int64_t>(j) * nsplit + sp;
-      const float w = __builtin_amdgcn_exp2f((part_ml[(unit * C::kQ + qloc) * 2] - m) * scale_log2);
+      const float w = __builtin_amdgcn_exp2f(part_ml[(unit * C::kQ + qloc) * 2] - m);
       lsum += w * part_ml[(unit * C::kQ + qloc) * 2 + 1];
       acc += w * part_o[unit * kUnit + o];
     }

@@ -256,6 +256,50 @@ def test_block_partial_attention_edges(w):
         check_block(got, want, w.dtype, f"{w.name}/{name}")
 
 
+def _reference_moves(q, k, H):
+    """Per (query, head) row: how often a lazily rescaled streaming softmax
+    moves its reference over the keys in 32-key halves (the reference starts
+    at the first half's maximum and moves when a half's largest exp2
+    argument exceeds it by more than 8), in fp64 from the oracle's q and k."""
+    dh = q.shape[1] // H
+    c = np.log2(np.e) / np.sqrt(dh)
+    moves = []
+    for h in range(H):
+        s = (q[:, h * dh:(h + 1) * dh] @ k[:, h * dh:(h + 1) * dh].T) * c
+        ref = s[:, :32].max(axis=1)
+        n = np.zeros(s.shape[0], np.int64)
+        for j in range(32, s.shape[1], 32):
+            m = s[:, j:j + 32].max(axis=1)
+            grow = m - ref > 8.0
+            ref = np.where(grow, m, ref)
+            n += grow
+        moves.append(n)
+    return np.concatenate(moves)
+
+
+def test_block_partial_attention_rescale():
+    """Peaked scores (query and key projections scaled by 10, score std about
+    10): most rows move their softmax reference along the keys, in waves that
+    also hold rows that do not move, which drives the attention's lazy
+    rescale path; the block matches the oracle as the other blocks do."""
+    w = synth.Workload("rescale_bf16_2600tok", T=5, grid=(20, 26), D=256, H=2, F=512,
+                       n_samples=4000, ratio=0.5, dtype="bf16", audio="bursts", seed=77)
+    p = synth.make_block_weights(w)
+    for name in ("wq", "wk"):
+        p[name] = synth.storage_round(p[name] * 10.0, w.dtype)
+    _, x = synth.make_latents(w)
+    kv = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    rng = np.random.default_rng(12)
+    idx = np.sort(rng.choice(w.L, 1000, replace=False))
+    q = OB.linear(kv[0][idx], OB._f64(p)["wq"], OB._f64(p)["bq"])
+    moves = _reference_moves(q, kv[1], w.H)
+    say(f"rescale: rows whose reference moves {np.mean(moves > 0):.2f}, moves per row up to {moves.max()}")
+    assert np.mean(moves > 0) > 0.5 and np.mean(moves == 0) > 0.01
+    got = _block_gpu(w, p, x, idx)
+    want = OB.block_partial(p, x, idx, w.H, kv=kv)
+    check_block(got, want, w.dtype, "rescale")
+
+
 def test_block_gates_one_informational():
     # gates ~ N(1, 0.1): larger bf16 error budget; reported, bounded loosely
     w = RAGGED
