@@ -778,6 +778,40 @@ def p720_leg(dev, dt, steps: int = 10):
             "data": "synthetic (seeded; 720p-shaped latents, random-init block weights, speech-like audio)"}
 
 
+def sustained_leg(out, kernels, work, w, args):
+    """The rate a dense bf16 MFMA stream sustains on this device with Gaussian
+    operands (A ~ N(0, 1), B ~ N(0, 0.02)) in the attention's and the GEMM's
+    instruction patterns (echo_mfma_ceiling), and the path's matrix kernels
+    against it: the nominal peak assumes a clock the part holds only while the
+    matrix cores switch few bits."""
+    from paper_2608_02474_amd import api, roofline
+    ceil = {pat: api.mfma_ceiling(pat, "gaussian", args.ceiling_secs) for pat in ("attention", "gemm")}
+    res = {"attention_pattern_tflops": round(ceil["attention"], 1), "gemm_pattern_tflops": round(ceil["gemm"], 1),
+           "attention_pattern_frac_of_peak": round(ceil["attention"] / roofline.PEAK_BF16_TFLOPS, 4),
+           "gemm_pattern_frac_of_peak": round(ceil["gemm"] / roofline.PEAK_BF16_TFLOPS, 4),
+           "seconds_each": args.ceiling_secs,
+           "what": "echo_mfma_ceiling: dense bf16 MFMAs with nothing else in the loop, Gaussian operands"}
+    per = {}
+    for name, k in kernels.items():
+        if k.get("unit") != "TFLOP/s":
+            continue
+        c = ceil["attention"] if name.startswith("attn_") else ceil["gemm"]
+        per[name] = round(k["achieved"] / c, 4)
+    res["kernels_frac_of_sustained"] = per
+    # the block's matrix work at the two sustained rates against its measured time
+    attn = roofline.work_of("attn_fwd_bf16", work)
+    attn_flop = attn[0] if attn else 0.0
+    gemm_flop = roofline.block_flops(w.L, w.K, w.D, w.F) - attn_flop
+    ideal_ms = (attn_flop / ceil["attention"] + gemm_flop / ceil["gemm"]) / 1e9
+    res["block_partial_frac_of_sustained"] = round(ideal_ms / out["block_partial"]["ms"], 4)
+    roof = out["roofline"]
+    c = ceil["attention"] if roof["kernel"].startswith("attn_") else ceil["gemm"]
+    if roof.get("unit") == "TFLOP/s" and roof.get("achieved"):
+        roof["sustained"] = round(c, 1)
+        roof["frac_of_sustained"] = round(roof["achieved"] / c, 4)
+    return res
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -799,6 +833,9 @@ def main() -> int:
                     help="timed steps of the 720p-shaped block leg; 0: skip")
     ap.add_argument("--dist-steps", type=int, default=50,
                     help="uninstrumented steps of the step-time distribution (at least --steps)")
+    ap.add_argument("--ceiling-secs", type=float, default=3.0,
+                    help="seconds of each sustained-MFMA-rate measurement (attention and GEMM "
+                         "instruction patterns on Gaussian operands); 0 leaves the leg out")
     ap.add_argument("--skip-cpu-baseline", action="store_true",
                     help="leave out the CPU oracle leg (profiler runs); the timed GPU step is "
                          "unchanged")
@@ -978,6 +1015,13 @@ def main() -> int:
         torch.cuda.empty_cache()
         out["p720"] = p720_leg(dev, dt, args.p720_steps)
         torch.cuda.empty_cache()
+
+    if args.ceiling_secs > 0:
+        log(f"sustained MFMA rate: attention and GEMM instruction patterns, Gaussian operands, "
+            f"{args.ceiling_secs:g} s each")
+        blk = None
+        torch.cuda.empty_cache()
+        out["mfma_sustained"] = sustained_leg(out, kernels, work, w, args)
 
     if args.skip_cpu_baseline:
         out["cpu_baseline"] = None

@@ -487,6 +487,32 @@ typedef struct {
 int echo_profile_enable(int on);
 int echo_profile_read(echo_kernel_time* out, int32_t max);
 
+/* ------------------------------------------------------ sustained MFMA rate */
+/*
+ * Diagnostic for the measurement of the matrix kernels, not part of the
+ * cached step.  The nominal bf16 peak (2516.6 TFLOP/s on a 256-CU part at
+ * 2.4 GHz) assumes the clock holds while the matrix cores work; it holds only
+ * while they switch few bits.  echo_mfma_ceiling runs a dense bf16 MFMA
+ * instruction stream with nothing else in its loop for `seconds` (after a
+ * warm-up of a third of that) and writes the sustained rate in TFLOP/s to
+ * *tflops: the ceiling the path's matrix kernels can reach on the same data.
+ *   pattern ECHO_MFMA_ATTENTION: 12 waves per CU, v_mfma_f32_32x32x16_bf16,
+ *           a new LDS operand for every MFMA (the attention's S and PV);
+ *   pattern ECHO_MFMA_GEMM: 4 waves per CU, 8 x 8 grids of
+ *           v_mfma_f32_16x16x32_bf16 tiles, 16 LDS fragment reads per 64
+ *           MFMAs (the four-wave GEMM without its global-to-LDS copies);
+ *   data ECHO_OPERANDS_CONSTANT: operands 1 + j/8;
+ *   data ECHO_OPERANDS_GAUSSIAN: A ~ N(0, 1), B ~ N(0, 0.02) rounded to bf16
+ *        (the path's activations and weights).
+ * Synchronous on `stream`; allocates a small result buffer on it.  Returns
+ * ECHO_EINVAL for an unknown pattern or data kind, seconds outside (0, 60]
+ * or a null tflops, ECHO_EDEVICE on a HIP error.
+ */
+typedef enum { ECHO_MFMA_ATTENTION = 0, ECHO_MFMA_GEMM = 1 } echo_mfma_pattern;
+typedef enum { ECHO_OPERANDS_CONSTANT = 0, ECHO_OPERANDS_GAUSSIAN = 1 } echo_operand_data;
+
+int echo_mfma_ceiling(int32_t pattern, int32_t data, double seconds, double* tflops, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -129,6 +129,7 @@ _SIGNATURES = {
                                             c_void_p, c_void_p]),
     "echo_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "echo_profile_read": (ctypes.c_int, [_P(KernelTime), c_int32]),
+    "echo_mfma_ceiling": (ctypes.c_int, [c_int32, c_int32, c_double, _P(c_double), c_void_p]),
 }
 
 _lib = None

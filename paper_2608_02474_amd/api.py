@@ -625,6 +625,19 @@ def profile_read(max_entries: int = 64) -> dict:
     return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms)) for i in range(n)}
 
 
+# ------------------------------------------------------ sustained MFMA rate
+
+def mfma_ceiling(pattern: str = "attention", data: str = "gaussian", seconds: float = 3.0) -> float:
+    """Sustained rate (TFLOP/s) of a dense bf16 MFMA stream with the attention's
+    ("attention") or the GEMM's ("gemm") instruction pattern on "gaussian" or
+    "constant" operands, on the current device and stream (echo_mfma_ceiling)."""
+    pat = {"attention": 0, "gemm": 1}[pattern]
+    dat = {"constant": 0, "gaussian": 1}[data]
+    out = ctypes.c_double(0.0)
+    check("echo_mfma_ceiling", _lib_handle().echo_mfma_ceiling(pat, dat, float(seconds), ctypes.byref(out), _stream()))
+    return out.value
+
+
 # ---------------------------------------------------------------- composition
 
 class CachedBlock:

@@ -21,7 +21,8 @@ LIB = os.path.join(HERE, "libecho.so")
 ARCH = "gfx950"
 
 SOURCES = ["echo_abi.cpp", "energy.hip", "select.hip", "cache.hip", "block_ln.hip",
-           "gemm_bf16.hip", "attn_bf16.hip", "block_f32.hip", "refcache.hip", "wan.hip"]
+           "gemm_bf16.hip", "attn_bf16.hip", "block_f32.hip", "refcache.hip", "wan.hip",
+           "mfma_ceiling.hip"]
 
 # Packed fp32 instructions are disabled for every device pass.
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

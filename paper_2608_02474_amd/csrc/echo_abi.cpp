@@ -724,6 +724,16 @@ int echo_refcache_update(const echo_refcache_cfg* cfg, const echo_refcache_state
       st->scale, xref, y, static_cast<hipStream_t>(stream)));
 }
 
+int echo_mfma_ceiling(int32_t pattern, int32_t data, double seconds, double* tflops, void* stream) {
+  if ((pattern != ECHO_MFMA_ATTENTION && pattern != ECHO_MFMA_GEMM) ||
+      (data != ECHO_OPERANDS_CONSTANT && data != ECHO_OPERANDS_GAUSSIAN) || !(seconds > 0.0 && seconds <= 60.0) ||
+      tflops == nullptr)
+    return ECHO_EINVAL;
+  const hipError_t e = run_mfma_ceiling(pattern, data == ECHO_OPERANDS_GAUSSIAN, seconds, tflops,
+                                        static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ECHO_OK : device_status(e);
+}
+
 int echo_profile_enable(int on) {
   profile_set(on != 0);
   return ECHO_OK;

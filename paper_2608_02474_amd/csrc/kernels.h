@@ -132,6 +132,8 @@ size_t attn_partial_bytes();
 size_t block_partial_bytes();
 // compute units of the current device (cached; 256 if the query fails)
 int device_cu_count();
+// sustained rate of a bf16 MFMA stream (pattern 0: attention, 1: GEMM; gaussian 0/1), TFLOP/s
+hipError_t run_mfma_ceiling(int pattern, int gaussian, double seconds, double* tflops, hipStream_t stream);
 hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, const float* v, int64_t ldkv,
                            int Mq, int L, int H, int dh, float* out, int64_t ldo, hipStream_t stream);
 

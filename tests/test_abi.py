@@ -85,6 +85,18 @@ def test_select_noalloc_rejects_before_launch(lib):
     assert lib.echo_status_str(_lib.ECHO_ELIMIT) == b"size above the allocation-free limit"
 
 
+def test_mfma_ceiling_rejects_before_launch(lib):
+    out = ctypes.c_double(-1.0)
+    run = lambda pat, dat, secs, o=ctypes.byref(out): lib.echo_mfma_ceiling(pat, dat, secs, o, None)
+    assert run(2, 1, 1.0) == _lib.ECHO_EINVAL                    # unknown pattern
+    assert run(0, 2, 1.0) == _lib.ECHO_EINVAL                    # unknown data kind
+    assert run(1, 1, 0.0) == _lib.ECHO_EINVAL                    # no time
+    assert run(1, 1, 61.0) == _lib.ECHO_EINVAL                   # above the limit
+    assert run(0, 0, float("nan")) == _lib.ECHO_EINVAL
+    assert run(0, 1, 1.0, None) == _lib.ECHO_EINVAL              # no output
+    assert out.value == -1.0
+
+
 def test_block_rejects_before_launch(lib):
     w = _lib.BlockWeights(*([0x20000] * 13))
     def run(cfg, n=4, wsb=1 << 40, weights=w):
