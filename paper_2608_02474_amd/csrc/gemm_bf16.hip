@@ -15,9 +15,12 @@
 // (one per SIMD) per tile, each wave a 128 x 128 quarter as 8 x 8 blocks of
 // v_mfma_f32_16x16x32_bf16, k-steps of 64 through a two-stage LDS ring that
 // direct global-to-LDS copies fill (gemm_bf16_w4 below).
-// Workgroup ids are remapped so that each XCD (blocks are dealt round-robin
-// to the 8 XCDs) owns a contiguous run of tiles, then grouped 8 tile-rows at
-// a time so a run shares A and B panels in its L2.  Tiles that do not fill a
+// Tiles are taken in a grouped order (8 tile-rows at a time, down the rows
+// first) and dealt so that the tiles running together on the 8 XCDs (blocks
+// go round-robin to the XCDs) form one block of 8 tile-rows: every L2 works
+// on the same A panels at the same time, which the memory-side cache then
+// serves once from HBM (each XCD streaming its own row panels fetched about
+// five times the algorithmic bytes from HBM on the K/V shape).  Tiles that do not fill a
 // last round of the device are split along k (gemm_splitk_reduce adds the
 // ranges in order and applies the epilogue).
 // Requires N % BN == 0, n_split % BN == 0, K % BK == 0 and byte offsets of
@@ -162,16 +165,23 @@ __global__ void __launch_bounds__(kW4Threads, 1) gemm_bf16_w4(GemmBf16Args p) {
   const int l16 = lane & 15, lq = lane >> 4;
 
   // ---- tile id.  Unsplit launches take tiles [tile_base, tile_base +
-  // gridDim.x) of the grouped order, remapped so that each XCD works through a
-  // contiguous run; split launches give workgroup g k-range g % nsplit of tile
-  // tile_base + g / nsplit.
+  // gridDim.x) of the grouped order, dealt to the XCDs as below; split
+  // launches give workgroup g k-range g % nsplit of tile tile_base + g /
+  // nsplit.
   const int tm = (p.M + BM - 1) / BM, tn = p.N / BN;
   const bool split_k = p.nsplit > 1;
   int pid, ksplit = 0;
   if (!split_k) {
-    const int total = gridDim.x, g = blockIdx.x;
-    const int q = total / 8, r = total % 8, xcd = g % 8, loc = g / 8;
-    pid = p.tile_base + xcd * q + (xcd < r ? xcd : r) + loc;
+    // workgroup g runs on XCD g % 8 as that XCD's (g / 8)-th; the XCDs'
+    // workgroups loc 32 w .. 32 w + 31 run together, so tile wave w of all
+    // eight XCDs takes grouped tiles 256 w .. 256 w + 255 (8 tile-rows x 32
+    // tile-columns), XCD x the 32 from 256 w + 32 x: the eight L2s work on
+    // the same A panels at the same time (shared through the memory-side
+    // cache) instead of each streaming its own; a last partial wave keeps the
+    // identity order
+    const int g = blockIdx.x, xcd = g % 8, loc = g / 8;
+    const int full_waves = gridDim.x / 256;
+    pid = p.tile_base + (loc < 32 * full_waves ? (loc / 32) * 256 + xcd * 32 + loc % 32 : g);
   } else {
     pid = p.tile_base + blockIdx.x / p.nsplit;
     ksplit = blockIdx.x % p.nsplit;
