@@ -18,9 +18,10 @@
 // Tiles are taken in a grouped order (8 tile-rows at a time, down the rows
 // first) and dealt so that the tiles running together on the 8 XCDs (blocks
 // go round-robin to the XCDs) form one block of 8 tile-rows: every L2 works
-// on the same A panels at the same time, which the memory-side cache then
-// serves once from HBM (each XCD streaming its own row panels fetched about
-// five times the algorithmic bytes from HBM on the K/V shape).  Tiles that do not fill a
+// on the same A panels at the same time, so that the misses of one L2 find
+// what another has just brought into the memory-side cache instead of going
+// to HBM (the L2s miss as often either way: about five times the algorithmic
+// bytes on the K/V shape).  Tiles that do not fill a
 // last round of the device are split along k (gemm_splitk_reduce adds the
 // ranges in order and applies the epilogue).
 // Requires N % BN == 0, n_split % BN == 0, K % BK == 0 and byte offsets of
