@@ -76,8 +76,10 @@ __device__ __forceinline__ void quantize8(const float* res, float inv, int8_t* d
 }
 
 // MAXC > 0: the fresh row's residual stays in registers (D <= 512 * MAXC);
-// MAXC == 0: the row is streamed twice (any D).
-template <typename T, int MAXC, int CODEC>
+// MAXC == 0: the row is streamed twice (any D).  FULL_ROWS (D = 512 MAXC:
+// every lane owns MAXC chunks) is a kernel of its own, so that the registers
+// of the ragged case do not count against it.
+template <typename T, int MAXC, int CODEC, bool FULL_ROWS = false>
 __global__ void __launch_bounds__(kCacheThreads)
 cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
                   const uint8_t* __restrict__ mask, int n_sel, int L, int D,
@@ -128,10 +130,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
           }
         }
       };
-      if (nch == R * kWave)
-        body(std::integral_constant<bool, true>{});
-      else
-        body(std::integral_constant<bool, false>{});
+      body(std::integral_constant<bool, FULL_ROWS>{});
     } else if constexpr (CODEC == kFull) {
       for (int c = lane; c < nch; c += kWave) {
         float yv[8];
@@ -234,10 +233,7 @@ cache_update_rows(const T* __restrict__ x, const int32_t* __restrict__ idx,
         if (FULL || c < nch) reuse8(rr[u], cw[u], c);
       }
     };
-    if (nch == R * kWave)
-      body(std::integral_constant<bool, true>{});
-    else
-      body(std::integral_constant<bool, false>{});
+    body(std::integral_constant<bool, FULL_ROWS>{});
   } else {
     for (int c = lane; c < nch; c += kWave) {
       Raw8<T> rr;
@@ -254,10 +250,14 @@ static hipError_t launch_cache_t(const char* name, const T* x, const int32_t* id
   const int64_t waves = static_cast<int64_t>(n_sel) + L;
   const dim3 grid(static_cast<unsigned>((waves + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
   const int per_lane = (D / 8 + kWave - 1) / kWave;
-#define ECHO_CACHE_CASE(MC)                                                                           \
-  if (per_lane <= MC)                                                                                 \
-    return ECHO_LAUNCH(name, (cache_update_rows<T, MC, CODEC>), grid, dim3(kCacheThreads), 0, stream, \
-                       x, idx, mask, n_sel, L, D, y_sel, xref, store, codes, scale, y);
+#define ECHO_CACHE_CASE(MC)                                                                                 \
+  if (per_lane <= MC) {                                                                                     \
+    if (D == 512 * MC)                                                                                      \
+      return ECHO_LAUNCH(name, (cache_update_rows<T, MC, CODEC, true>), grid, dim3(kCacheThreads), 0, stream, \
+                         x, idx, mask, n_sel, L, D, y_sel, xref, store, codes, scale, y);                   \
+    return ECHO_LAUNCH(name, (cache_update_rows<T, MC, CODEC, false>), grid, dim3(kCacheThreads), 0, stream,  \
+                       x, idx, mask, n_sel, L, D, y_sel, xref, store, codes, scale, y);                     \
+  }
   ECHO_CACHE_CASE(1)
   ECHO_CACHE_CASE(2)
   ECHO_CACHE_CASE(3)
