@@ -507,6 +507,10 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     }
     // chunk NPRE + j: exp2 after S MFMA 8 j / NJ, pack and row sum after the next
     float tq[2][QB][2];
+    // the wave's S phase (with the exp work of the half before) at a higher
+    // issue priority than the PV phases of the other waves on its SIMD
+    // (0.5% faster; the reverse was 1.3% slower)
+    __builtin_amdgcn_s_setprio(2);
     s_half(smem + STN * ATT_TILE_BYTES, KBN, sn, [&](int i) __attribute__((always_inline)) {
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
@@ -535,6 +539,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restric
     // S_{h+1}: arguments of chunks 0 .. NPRE - 1 after PV MFMA 0, their exp2
     // after MFMAs 2 .., each pack one MFMA later (the first four PV MFMAs read
     // the packed keys 0-15); the other arguments after MFMAs 4-7
+    __builtin_amdgcn_s_setprio(0);
     pv_half(smem + ST * ATT_TILE_BYTES, KB, pf, [&](int i) __attribute__((always_inline)) {
       if (i == 0) {
 #pragma unroll
