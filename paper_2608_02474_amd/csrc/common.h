@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace echo {
 
 typedef uint16_t bf16_t;                                            // storage
@@ -132,20 +134,59 @@ template <> struct Raw8<float> {
   }
 };
 
-// wave64 reductions (every lane gets the result)
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+// wave64 reductions (every lane gets the result).  The partner at lane
+// distance 32 and 16 comes from the gfx950 lane swaps (v_permlane32_swap,
+// v_permlane16_swap: both halves of a pair in two registers), those at 8, 4,
+// 2 and 1 from DPP row rotations inside the 16-lane rows, which the adder
+// reads directly.  In this descending order the lane a rotation by d reaches
+// holds the same value as lane i ^ d (after the steps above it, lanes that
+// differ only in the bits above d's are equal), so every lane adds exactly
+// the operands of an xor butterfly 32, 16, .., 1 and all lanes end with the
+// same bits.  No LDS traffic: a ds_bpermute butterfly costs six LDS round
+// trips per reduction.
+template <int D>
+__device__ __forceinline__ uint32_t dpp_ror(uint32_t v) {
+  static_assert(D == 1 || D == 2 || D == 4 || D == 8, "row rotation by 1, 2, 4 or 8");
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x120 + D, 0xf, 0xf, false));
+}
+template <typename Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = op(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = op(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  v = op(v, __uint_as_float(dpp_ror<8>(__float_as_uint(v))));
+  v = op(v, __uint_as_float(dpp_ror<4>(__float_as_uint(v))));
+  v = op(v, __uint_as_float(dpp_ror<2>(__float_as_uint(v))));
+  v = op(v, __uint_as_float(dpp_ror<1>(__float_as_uint(v))));
   return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
 }
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  auto swap = [](double x, auto perm) {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+    const auto lo = perm(static_cast<uint32_t>(u)), hi = perm(static_cast<uint32_t>(u >> 32));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi[0]) << 32) | lo[0])) +
+           __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi[1]) << 32) | lo[1]));
+  };
+  v = swap(v, [](uint32_t w) { return __builtin_amdgcn_permlane32_swap(w, w, false, false); });
+  v = swap(v, [](uint32_t w) { return __builtin_amdgcn_permlane16_swap(w, w, false, false); });
+  auto ror = [](double x, auto d_c) {
+    constexpr int D = decltype(d_c)::value;
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+    const uint64_t r = (static_cast<uint64_t>(dpp_ror<D>(static_cast<uint32_t>(u >> 32))) << 32) |
+                       dpp_ror<D>(static_cast<uint32_t>(u));
+    return x + __longlong_as_double(static_cast<long long>(r));
+  };
+  v = ror(v, std::integral_constant<int, 8>{});
+  v = ror(v, std::integral_constant<int, 4>{});
+  v = ror(v, std::integral_constant<int, 2>{});
+  v = ror(v, std::integral_constant<int, 1>{});
   return v;
 }
 
