@@ -66,11 +66,7 @@ int device_cu_count() {
   return n;
 }
 
-size_t block_partial_bytes() {
-  const size_t gemm = sizeof(float) * 256 * 256 * 256;  // 256 fp32 tiles of 256 x 256
-  const size_t attn = attn_partial_bytes();
-  return gemm > attn ? gemm : attn;
-}
+size_t gemm_partial_bytes() { return sizeof(float) * 256 * 256 * 256; }
 
 }  // namespace echo
 
@@ -184,9 +180,11 @@ bool block_supported(const echo_block_cfg* c) {
 struct BlockWs {
   void *a, *kv, *q, *o, *b, *h;
   float* x1;
-  float* part;  // bf16 path: partial results of the key-split attention tail
+  float* part;        // bf16 path: partial results of the GEMM and attention tails
+  size_t part_bytes;  // its size: the larger of the two needs
   size_t bytes;
 };
+size_t max_size(size_t a, size_t b) { return a > b ? a : b; }
 BlockWs block_ws_layout(const echo_block_cfg* c, int64_t n, char* base) {
   const size_t es = esize(c->dtype);
   const size_t L = c->L, D = c->D, F = c->F, m = static_cast<size_t>(n);
@@ -204,7 +202,10 @@ BlockWs block_ws_layout(const echo_block_cfg* c, int64_t n, char* base) {
   w.x1 = reinterpret_cast<float*>(take(m * D * 4));
   w.b = take(m * D * es);
   w.h = take(m * F * es);
-  if (c->dtype == ECHO_BF16) w.part = reinterpret_cast<float*>(take(block_partial_bytes()));
+  if (c->dtype == ECHO_BF16) {
+    w.part_bytes = max_size(gemm_partial_bytes(), attn_partial_bytes(static_cast<int>(n), c->L, c->H));
+    w.part = reinterpret_cast<float*>(take(w.part_bytes));
+  }
   w.bytes = off;
   return w;
 }
@@ -246,6 +247,7 @@ struct WanWs {
   void *a, *kv, *kvc, *q, *o, *b, *h;
   float *x1, *x2, *part, *ones, *g3m1;
   float2* tab;
+  size_t part_bytes;
   size_t bytes;
 };
 WanWs wan_ws_layout(const echo_wan_block_cfg* c, int64_t n, char* base) {
@@ -267,7 +269,11 @@ WanWs wan_ws_layout(const echo_wan_block_cfg* c, int64_t n, char* base) {
   w.h = take(m * F * es);
   w.x1 = reinterpret_cast<float*>(take(m * D * 4));
   w.x2 = reinterpret_cast<float*>(take(m * D * 4));
-  w.part = reinterpret_cast<float*>(take(block_partial_bytes()));
+  // the attention runs per batch element, with at most n selected rows
+  w.part_bytes = max_size(gemm_partial_bytes(),
+                          max_size(attn_partial_bytes(static_cast<int>(n), c->L, c->H),
+                                   attn_partial_bytes(static_cast<int>(n), c->Lc, c->H)));
+  w.part = reinterpret_cast<float*>(take(w.part_bytes));
   w.ones = reinterpret_cast<float*>(take(D * 4));
   w.g3m1 = reinterpret_cast<float*>(take(D * 4));
   w.tab = reinterpret_cast<float2*>(take(sizeof(float2) * size_t(rope_table_entries(c->T, c->gh, c->gw,
@@ -487,7 +493,7 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
     float* part = (cfg->flags & ECHO_BLOCK_BATCH_INVARIANT) ? nullptr : ws.part;
     auto with_part = [&](GemmBf16Args a) {
       a.part = part;
-      a.part_bytes = block_partial_bytes();
+      a.part_bytes = ws.part_bytes;
       return a;
     };
     // q = a[idx] Wq^T + bq
@@ -503,7 +509,7 @@ int echo_block_partial(const echo_block_cfg* cfg, const echo_block_weights* w, c
     const bf16_t* kvp = static_cast<const bf16_t*>(ws.kv);
     if ((e = launch_attn_bf16(static_cast<P>(ws.q), D, kvp, kvp + D, 2 * D, n, L, H,
                               static_cast<bf16_t*>(ws.o), D,
-                              part, block_partial_bytes(), st)) !=
+                              part, ws.part_bytes, st)) !=
         hipSuccess)
       return device_status(e);
     // x1 = x[idx] + gate1 * (o Wo^T + bo)
@@ -589,7 +595,7 @@ int echo_wan_block_partial(const echo_wan_block_cfg* cfg, const echo_wan_block_w
   float* part = (cfg->flags & ECHO_BLOCK_BATCH_INVARIANT) ? nullptr : ws.part;
   auto with_part = [&](GemmBf16Args a) {
     a.part = part;
-    a.part_bytes = block_partial_bytes();
+    a.part_bytes = ws.part_bytes;
     return a;
   };
   hipError_t e;
@@ -620,7 +626,7 @@ int echo_wan_block_partial(const echo_wan_block_cfg* cfg, const echo_wan_block_w
     for (int b = 0; b < B; ++b) {
       const bf16_t* kb = kvp + int64_t(b) * L * 2 * D;
       ECHO_TRY(launch_attn_bf16(static_cast<P>(ws.q) + o * D, D, kb, kb + D, 2 * D, n_sel[b], L, H,
-                                static_cast<bf16_t*>(ws.o) + o * D, D, part, block_partial_bytes(), st));
+                                static_cast<bf16_t*>(ws.o) + o * D, D, part, ws.part_bytes, st));
       o += n_sel[b];
     }
   }
@@ -648,7 +654,7 @@ int echo_wan_block_partial(const echo_wan_block_cfg* cfg, const echo_wan_block_w
     for (int b = 0; b < B; ++b) {
       const bf16_t* kb = kvp + int64_t(b) * Lc * 2 * D;
       ECHO_TRY(launch_attn_bf16(static_cast<P>(ws.q) + o * D, D, kb, kb + D, 2 * D, n_sel[b], Lc, H,
-                                static_cast<bf16_t*>(ws.o) + o * D, D, part, block_partial_bytes(), st,
+                                static_cast<bf16_t*>(ws.o) + o * D, D, part, ws.part_bytes, st,
                                 "attn_cross_bf16"));
       o += n_sel[b];
     }

@@ -120,16 +120,18 @@ hipError_t launch_modln_x1(int dtype_bf16, const float* x1, int M, int D, const 
 hipError_t launch_gemm_bf16(const char* name, int epi, const GemmBf16Args& a, hipStream_t stream);
 hipError_t launch_gemm_f32(const char* name, int epi, const GemmF32Args& a, hipStream_t stream);
 
-// `part` (part_bytes, attn_partial_bytes() is enough) holds the partial
-// results of the key-split tail work items; with part == nullptr nothing is split.
+// `part` (part_bytes; attn_partial_bytes(Mq_max, L, H) is enough for any Mq
+// up to Mq_max) holds the partial results of the key-range pieces that
+// balance the last round; with part == nullptr, or less room, every work item
+// runs whole.
 hipError_t launch_attn_bf16(const bf16_t* q, int64_t ldq, const bf16_t* k, const bf16_t* v,
                             int64_t ldkv, int Mq, int L, int H, bf16_t* out, int64_t ldo,
                             float* part, size_t part_bytes, hipStream_t stream,
                             const char* timing_name = "attn_fwd_bf16");
-size_t attn_partial_bytes();
-// bytes that hold the partial results of any split tail of the bf16 block
-// (attention key splits, GEMM k splits): 256 units of the larger kind
-size_t block_partial_bytes();
+size_t attn_partial_bytes(int Mq_max, int L, int H);
+// bytes that hold the partial results of the GEMMs' split tails (256 fp32
+// tiles of 256 x 256)
+size_t gemm_partial_bytes();
 // compute units of the current device (cached; 256 if the query fails)
 int device_cu_count();
 // sustained rate of a bf16 MFMA stream (pattern 0: attention, 1: GEMM; gaussian 0/1), TFLOP/s
