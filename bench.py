@@ -833,6 +833,9 @@ def main() -> int:
                     help="timed steps of the 720p-shaped block leg; 0: skip")
     ap.add_argument("--dist-steps", type=int, default=50,
                     help="uninstrumented steps of the step-time distribution (at least --steps)")
+    ap.add_argument("--dense-steps", type=int, default=None,
+                    help="timed calls of the dense block over every token (default: --steps); 0 leaves "
+                         "the leg out (profiler runs: its launches would share grids with the cached step's)")
     ap.add_argument("--ceiling-secs", type=float, default=3.0,
                     help="seconds of each sustained-MFMA-rate measurement (attention and GEMM "
                          "instruction patterns on Gaussian operands); 0 leaves the leg out")
@@ -899,13 +902,20 @@ def main() -> int:
 
     # the plain dense block over every token (no selection, no cache update):
     # the denominator of the cached step's speedup
-    log(f"dense block: {args.steps} calls over all {w.L} tokens")
+    n_dense = args.steps if args.dense_steps is None else args.dense_steps
+    dense_out = None
+    if n_dense > 0:
+        log(f"dense block: {n_dense} calls over all {w.L} tokens")
 
-    def dense():
-        api.block_partial(P, X, blk.all_idx, w.L, w.H, y_sel=blk.y_sel, workspace=blk.ws, _weights=blk._w)
-    dense()
-    dense_total, dense_steps = _per_step_times(dense, args.steps)
-    dense_ms = dense_total / args.steps
+        def dense():
+            api.block_partial(P, X, blk.all_idx, w.L, w.H, y_sel=blk.y_sel, workspace=blk.ws, _weights=blk._w)
+        dense()
+        dense_total, _ = _per_step_times(dense, n_dense)
+        dense_ms = dense_total / n_dense
+        dense_out = {"ms": round(dense_ms, 4), "tokens_per_s": round(w.L / (dense_ms * 1e-3), 1),
+                     "tflops": round(roofline.block_flops(w.L, w.L, w.D, w.F) / (dense_ms * 1e-3) / 1e12, 2),
+                     "speedup_of_cached_step": round(dense_ms / ms, 3),
+                     "what": "echo_block_partial over all L tokens (no selection, no cache update)"}
 
     # per-kernel times from a separate, instrumented run of the same steps
     log(f"per-kernel timing: {args.steps} instrumented steps")
@@ -965,10 +975,7 @@ def main() -> int:
                             "uninstrumented steps; instrumented_mean: the per-kernel run with two HIP "
                             "events per launch"},
         "clock": dict(clock_summary, during="the distribution steps"),
-        "dense_block": {"ms": round(dense_ms, 4), "tokens_per_s": round(w.L / (dense_ms * 1e-3), 1),
-                        "tflops": round(roofline.block_flops(w.L, w.L, w.D, w.F) / (dense_ms * 1e-3) / 1e12, 2),
-                        "speedup_of_cached_step": round(dense_ms / ms, 3),
-                        "what": "echo_block_partial over all L tokens (no selection, no cache update)"},
+        "dense_block": dense_out,
         "roofline": roof,
         "block_partial": {"ms": round(block_ms, 4), "tflops": round(block_tf, 2),
                           "frac_bf16_peak": round(block_tf / roofline.PEAK_BF16_TFLOPS, 4)},

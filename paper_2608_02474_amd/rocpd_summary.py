@@ -20,6 +20,10 @@ with its default output format).
 
 Grouping by grid size separates dispatches of one kernel at different
 problem sizes (for example the all-token first step from the cached steps).
+`--skip-first N` (any mode) leaves out the first N dispatches of every
+(kernel, grid size), in dispatch order: a launch of the cached block's
+all-token first step that has the grid of a cached step's launch (the
+attention's 256 key ranges) then does not enter the cached step's figures.
 """
 from __future__ import annotations
 
@@ -30,6 +34,34 @@ import sqlite3
 import sys
 
 COPY_BYTES = 1 << 30  # what the hbm_copy module reads and writes by default
+SKIP = 0  # dispatches left out at the start of every (kernel, grid size)
+
+
+def _order_column(c, view: str) -> str:
+    """A column of `view` that orders dispatches in time."""
+    cols = [d[0] for d in c.execute(f"select * from {view} limit 0").description]
+    for name in ("start", "dispatch_id", "id"):
+        if name in cols:
+            return name
+    raise SystemExit(f"no ordering column (start, dispatch_id, id) in {view}: {cols}")
+
+
+def _kernels(c) -> str:
+    """The kernels view, less the first SKIP dispatches of every (kernel, grid)."""
+    if SKIP <= 0:
+        return "kernels"
+    o = _order_column(c, "kernels")
+    return (f"(select * from (select *, row_number() over (partition by name, grid_x, grid_y, grid_z "
+            f"order by {o}) as skip_rn from kernels) where skip_rn > {SKIP})")
+
+
+def _counters(c) -> str:
+    """The counters view, less the first SKIP dispatches of every (kernel, grid, counter)."""
+    if SKIP <= 0:
+        return "counters_collection"
+    o = _order_column(c, "counters_collection")
+    return (f"(select * from (select *, row_number() over (partition by kernel_name, grid_size, counter_name "
+            f"order by {o}) as skip_rn from counters_collection) where skip_rn > {SKIP})")
 
 
 def short_name(n: str) -> str:
@@ -40,7 +72,7 @@ def short_name(n: str) -> str:
 def trace_rows(db: str):
     c = sqlite3.connect(db)
     q = ("select name, grid_x * grid_y * grid_z, count(*), avg(duration), min(duration), "
-         "max(duration), sum(duration) from kernels group by name, grid_x, grid_y, grid_z "
+         f"max(duration), sum(duration) from {_kernels(c)} group by name, grid_x, grid_y, grid_z "
          "order by sum(duration) desc")
     return [(short_name(r[0]), r[1], r[2], r[3] / 1e3, r[4] / 1e3, r[5] / 1e3, r[6] / 1e3)
             for r in c.execute(q)]
@@ -48,14 +80,14 @@ def trace_rows(db: str):
 
 def counter_rows(db: str, counter: str):
     c = sqlite3.connect(db)
-    q = ("select kernel_name, grid_size, count(*), avg(value) from counters_collection "
+    q = (f"select kernel_name, grid_size, count(*), avg(value) from {_counters(c)} "
          "where counter_name = ? group by kernel_name, grid_size order by avg(value) desc")
     return [(short_name(r[0]), r[1], r[2], r[3]) for r in c.execute(q, (counter,))]
 
 
 def counter_of(db: str, counter: str, substring: str, grid: int) -> float:
     c = sqlite3.connect(db)
-    q = ("select avg(value) from counters_collection where counter_name = ? and "
+    q = (f"select avg(value) from {_counters(c)} where counter_name = ? and "
          "kernel_name like ? and grid_size = ?")
     v = c.execute(q, (counter, f"%{substring}%", grid)).fetchone()[0]
     if v is None:
@@ -97,7 +129,7 @@ def dispatch_durations(db: str):
     of a run (empty if the run recorded none)."""
     c = sqlite3.connect(db)
     try:
-        q = ("select name, grid_x * grid_y * grid_z, avg(duration) from kernels "
+        q = (f"select name, grid_x * grid_y * grid_z, avg(duration) from {_kernels(c)} "
              "group by name, grid_x, grid_y, grid_z")
         return {(short_name(r[0]), r[1]): r[2] for r in c.execute(q)}
     except sqlite3.Error:
@@ -112,7 +144,7 @@ def counter_table(dbs, pattern: str = ""):
     for db in dbs:
         dur = dispatch_durations(db)
         c = sqlite3.connect(db)
-        q = ("select kernel_name, grid_size, counter_name, count(*), avg(value) from counters_collection "
+        q = (f"select kernel_name, grid_size, counter_name, count(*), avg(value) from {_counters(c)} "
              "where kernel_name like ? group by kernel_name, grid_size, counter_name")
         for name, grid, counter, n, v in c.execute(q, (f"%{pattern}%",)):
             key = (short_name(name), grid)
@@ -159,6 +191,11 @@ def mfma_summary(dbs, pattern: str = "", simds: int = 1024, xcds: int = 8):
 
 
 def main(argv):
+    global SKIP
+    if "--skip-first" in argv:
+        i = argv.index("--skip-first")
+        SKIP = int(argv[i + 1])
+        argv = argv[:i] + argv[i + 2:]
     if len(argv) >= 2 and argv[0] == "trace":
         print(f"{'kernel':58s} {'grid threads':>12s} {'calls':>5s} {'avg us':>10s} "
               f"{'min us':>10s} {'max us':>10s} {'total us':>11s}")
