@@ -256,6 +256,31 @@ def test_block_partial_attention_edges(w):
         check_block(got, want, w.dtype, f"{w.name}/{name}")
 
 
+# bf16 shapes whose attention runs the balanced key ranges (at least 32 key
+# tiles): few items, so that every item is cut into many pieces merged by the
+# combine; query counts that leave the last query tile of a head with 48, 160
+# and 288 queries (one, two and three waves with queries on the busiest
+# SIMD: the three costs of a short item), whole tiles only, and every token;
+# the 2100-token shape ends in a ragged key tile
+BALANCED = [synth.Workload(f"balanced_bf16_{T * gh * gw}tok", T=T, grid=(gh, gw), D=256, H=2, F=512,
+                           n_samples=8000, ratio=0.3, dtype="bf16", audio="speech", seed=70 + T)
+            for T, gh, gw in [(5, 16, 32), (3, 20, 35)]]
+
+
+@pytest.mark.parametrize("w", BALANCED, ids=lambda w: w.name)
+def test_block_partial_balanced_ranges(w):
+    p = synth.make_block_weights(w)
+    _, x = synth.make_latents(w)
+    rng = np.random.default_rng(13)
+    kv = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    for n in (48, 432, 544, 672, 768, w.L):
+        idx = np.sort(rng.choice(w.L, n, replace=False))
+        say(f"block {w.name} n={n}")
+        got = _block_gpu(w, p, x, idx)
+        want = OB.block_partial(p, x, idx, w.H, kv=kv)
+        check_block(got, want, w.dtype, f"{w.name}/n={n}")
+
+
 def _reference_moves(q, k, H):
     """Per (query, head) row: how often a lazily rescaled streaming softmax
     moves its reference over the keys in 32-key halves (the reference starts
