@@ -8,7 +8,9 @@
 // fp32 with two passes over the registers, and the modulated result is
 // written in the output storage type.  Every access, the modulation vectors
 // included, is a 16-byte vector load or store.  Rows longer than 512 * MAXC
-// elements take the MAXC == 0 variant, which re-reads the row.
+// elements take the MAXC == 0 variant, which re-reads the row.  fp32 rows of
+// a width that is a multiple of 512 (the second LayerNorm) are shared by the
+// waves of a workgroup instead (modln_rows_wg).
 #include <type_traits>
 
 #include "common.h"
@@ -239,10 +241,95 @@ modln_rows_lds(const Tin* __restrict__ x, int M, int D, const float* __restrict_
     body(std::integral_constant<bool, FULL_ROWS>{}, x + row * D, out + row * D);
 }
 
+
+// fp32 rows (the second LayerNorm, over x1) are shared by a workgroup instead:
+// WAVES = D / 512 waves, each thread one 8-element chunk (c = threadIdx.x),
+// whose modulation it keeps in registers for every row it takes.  The
+// workgroup loops over rows and issues the next row's loads before the
+// current row's two reductions (each a wave sum, then the WAVES partial sums
+// added in wave order from LDS).  With a wave per row (the kernel above) each
+// wave keeps 20 KB of a 5120-wide fp32 row in flight and the second LayerNorm
+// ran at 0.67 of HBM; this form keeps 32 bytes per thread and the next row
+// in flight (75.3 -> 71.1 us on 13104 x 5120 rows, 0.71 of HBM).  It does not
+// help bf16 rows (the first LayerNorm).
+template <typename Tin, typename Tout, int WAVES>
+__global__ void __launch_bounds__(WAVES * 64)
+modln_rows_wg(const Tin* __restrict__ x, int M, int D, const float* __restrict__ shift,
+              const float* __restrict__ scale, float eps, Tout* __restrict__ out) {
+  __shared__ float red[2][WAVES];  // per-wave partial sums: [0] the row sum, [1] the squared deviations
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const float invD = 1.0f / static_cast<float>(D);
+  float a[8], b[8];
+  ln_load8(scale + tid * 8, a);
+  ln_load8(shift + tid * 8, b);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) a[j] += 1.0f;
+  int row = blockIdx.x;  // gridDim.x <= M
+  Raw8<Tin> cur, nxt;
+  cur.load_nt(x + static_cast<int64_t>(row) * D + tid * 8);
+  for (; row < M; row += gridDim.x) {
+    const int nrow = row + gridDim.x;
+    if (nrow < M) nxt.load_nt(x + static_cast<int64_t>(nrow) * D + tid * 8);
+    float v[8];
+    cur.unpack(v);
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += v[j];
+    s = wave_sum(s);
+    if (lane == 0) red[0][wave] = s;
+    // (a slot is written again only after the next barrier, which every
+    // reader of this row's value reaches after its read)
+    __syncthreads();
+    s = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) s += red[0][w];
+    const float mean = s * invD;
+    float sq = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float d = v[j] - mean;
+      sq += d * d;
+    }
+    sq = wave_sum(sq);
+    if (lane == 0) red[1][wave] = sq;
+    __syncthreads();
+    sq = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) sq += red[1][w];
+    const float rstd = 1.0f / sqrtf(sq * invD + eps);
+    float o[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = (v[j] - mean) * rstd * a[j] + b[j];
+    ln_store8(out + static_cast<int64_t>(row) * D + tid * 8, o);
+    cur = nxt;
+  }
+}
+
+template <typename Tin, typename Tout, int WAVES>
+static hipError_t launch_modln_wg(const char* name, const Tin* x, int M, int D, const float* shift,
+                                  const float* scale, float eps, Tout* out, hipStream_t stream) {
+  // about 20 waves per CU (two workgroups at D = 5120: one or three were slower)
+  const int per_cu = WAVES < 10 ? 20 / WAVES : 2;
+  const int cap = per_cu * device_cu_count();
+  const dim3 grid(static_cast<unsigned>(M < cap ? M : cap));
+  return ECHO_LAUNCH(name, (modln_rows_wg<Tin, Tout, WAVES>), grid, dim3(WAVES * 64), 0, stream, x, M, D,
+                     shift, scale, eps, out);
+}
+
 template <typename Tin, typename Tout>
 static hipError_t launch_modln_t(const char* name, const Tin* x, int M, int D, const float* shift,
                                  const float* scale, float eps, Tout* out, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
+  if (std::is_same<Tin, float>::value && D % 512 == 0) {
+    switch (D / 512) {
+      case 4: return launch_modln_wg<Tin, Tout, 4>(name, x, M, D, shift, scale, eps, out, stream);
+      case 8: return launch_modln_wg<Tin, Tout, 8>(name, x, M, D, shift, scale, eps, out, stream);
+      case 10: return launch_modln_wg<Tin, Tout, 10>(name, x, M, D, shift, scale, eps, out, stream);
+      case 12: return launch_modln_wg<Tin, Tout, 12>(name, x, M, D, shift, scale, eps, out, stream);
+      case 16: return launch_modln_wg<Tin, Tout, 16>(name, x, M, D, shift, scale, eps, out, stream);
+      default: break;
+    }
+  }
   const dim3 grid((M + kLnWaves - 1) / kLnWaves);
   const int per_lane = (D / 8 + kWave - 1) / kWave;
   if (D <= kLnLdsMaxD) {

@@ -22,8 +22,8 @@
 // what another has just brought into the memory-side cache instead of going
 // to HBM (the L2s miss as often either way: about five times the algorithmic
 // bytes on the K/V shape).  Tiles that do not fill a
-// last round of the device are split along k (gemm_splitk_reduce adds the
-// ranges in order and applies the epilogue).
+// last round of the device are split along k, run first in the same launch
+// (gemm_splitk_reduce adds the ranges in order and applies the epilogue).
 // Requires N % BN == 0, n_split % BN == 0, K % BK == 0 and byte offsets of
 // A and B rows below 2^31; M is arbitrary (tail rows clamp their loads and
 // skip their stores).
@@ -170,12 +170,11 @@ __global__ void __launch_bounds__(kW4Threads, 1) gemm_bf16_w4(GemmBf16Args p) {
   const int wm = wave >> 1, wn = wave & 1;
   const int l16 = lane & 15, lq = lane >> 4;
 
-  // ---- tile id.  Unsplit launches take tiles [tile_base, tile_base +
-  // gridDim.x) of the grouped order, dealt to the XCDs as below; split
-  // launches give workgroup g k-range g % nsplit of tile tile_base + g /
-  // nsplit.
+  // ---- tile id.  Workgroups g < npieces are k-split pieces: k-range
+  // g % nsplit of tile tile_base + g / nsplit.  The rest take whole tiles
+  // [0, gridDim.x - npieces) of the grouped order, dealt to the XCDs as below.
   const int tm = (p.M + BM - 1) / BM, tn = p.N / BN;
-  const bool split_k = p.nsplit > 1;
+  const bool split_k = static_cast<int>(blockIdx.x) < p.npieces;
   int pid, ksplit = 0;
   if (!split_k) {
     // workgroup g runs on XCD g % 8 as that XCD's (g / 8)-th; the XCDs'
@@ -185,9 +184,9 @@ __global__ void __launch_bounds__(kW4Threads, 1) gemm_bf16_w4(GemmBf16Args p) {
     // the same A panels at the same time (shared through the memory-side
     // cache) instead of each streaming its own; a last partial wave keeps the
     // identity order
-    const int g = blockIdx.x, xcd = g % 8, loc = g / 8;
-    const int full_waves = gridDim.x / 256;
-    pid = p.tile_base + (loc < 32 * full_waves ? (loc / 32) * 256 + xcd * 32 + loc % 32 : g);
+    const int g = blockIdx.x - p.npieces, xcd = g % 8, loc = g / 8;
+    const int full_waves = (gridDim.x - p.npieces) / 256;
+    pid = loc < 32 * full_waves ? (loc / 32) * 256 + xcd * 32 + loc % 32 : g;
   } else {
     pid = p.tile_base + blockIdx.x / p.nsplit;
     ksplit = blockIdx.x % p.nsplit;
@@ -340,16 +339,18 @@ __global__ void __launch_bounds__(kW4Threads, 1) gemm_bf16_w4(GemmBf16Args p) {
   // Gate + residual: the residual rows of group i are the lane's rows
   // m0 + wm 128 + 16 i + 2 q + lane / 32 (q < 8), gathered through res_rows
   // if given.  bf16 residuals (the O projection's gathered block input) are
-  // fetched one group ahead, their row indices two groups ahead, so that the
-  // latency hides behind the staging and stores of the group before (O
-  // projection 0.599 -> 0.583 ms); fp32 residuals (read once, no gather)
-  // are fetched at the start of their group, where the prefetch gained
-  // nothing and cost registers.
+  // fetched NPF = 2 groups ahead, their row indices three groups ahead, so
+  // that the latency hides behind the staging and stores of the groups
+  // before (O projection: no prefetch 0.599 ms, one group 0.583 - 0.600, two
+  // groups 8 us less, three or four no better); fp32 residuals (read once, no
+  // gather) are fetched at the start of their group, where the prefetch
+  // gained nothing and cost registers.
   constexpr bool RES = EPI == EPI_GATE_RES;
   constexpr int NQ = RES ? 8 : 1;
   const bool pre = RES && !split_k && p.res_bf16;
-  int32_t rrow[2][NQ];
-  uint2 rawb[2][NQ];
+  constexpr int NPF = 2, NS = NPF + 1;
+  int32_t rrow[2][NQ];  // row indices of groups g in slot g % 2
+  uint2 rawb[NS][NQ];   // residuals of group g in slot g % NS
   auto rows_of = [&](int i, int32_t(&dst)[NQ]) __attribute__((always_inline)) {
     if constexpr (RES) {
 #pragma unroll
@@ -371,22 +372,26 @@ __global__ void __launch_bounds__(kW4Threads, 1) gemm_bf16_w4(GemmBf16Args p) {
     }
   };
   if (pre) {
-    rows_of(0, rrow[0]);
-    rows_of(1, rrow[1]);
-    load_bf16(rrow[0], rawb[0]);
+#pragma unroll
+    for (int g = 0; g < NPF; ++g) {
+      rows_of(g, rrow[g % 2]);
+      load_bf16(rrow[g % 2], rawb[g]);
+    }
+    rows_of(NPF, rrow[NPF % 2]);
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     float res[NR][4];
     if constexpr (RES) {
       if (pre) {
-        // rrow[(i + 1) % 2] holds group i + 1's rows: issue its residuals,
-        // then fetch the rows of group i + 2 into the slot group i used
-        if (i + 1 < 8) load_bf16(rrow[(i + 1) % 2], rawb[(i + 1) % 2]);
-        if (i + 2 < 8) rows_of(i + 2, rrow[i % 2]);
+        // issue the residuals of group i + NPF (its rows are in slot
+        // (i + NPF) % 2), then fetch the rows of group i + NPF + 1 into the
+        // other slot, whose group's residuals were issued the group before
+        if (i + NPF < 8) load_bf16(rrow[(i + NPF) % 2], rawb[(i + NPF) % NS]);
+        if (i + NPF + 1 < 8) rows_of(i + NPF + 1, rrow[(i + NPF + 1) % 2]);
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-          const uint2 v = rawb[i % 2][q];
+          const uint2 v = rawb[i % NS][q];
           res[q][0] = __uint_as_float(v.x << 16);
           res[q][1] = __uint_as_float(v.x & 0xffff0000u);
           res[q][2] = __uint_as_float(v.y << 16);
@@ -487,6 +492,7 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   if (a.part == nullptr) nsplit = 1;
   ::echo::TimedLaunch scope(name, stream);
   a.tile_base = 0;
+  a.npieces = 0;
   if (nsplit < 2) {
     a.nsplit = 1;
     KERNEL::launch(tiles, a, stream);
@@ -494,16 +500,16 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   }
   a.kps = (nk + nsplit - 1) / nsplit;  // k-steps per split
   nsplit = (nk + a.kps - 1) / a.kps;   // every split non-empty
+  // One launch, the pieces first: when they cover only part of the CUs (the
+  // 13104-row projections: 16 tiles x 8 pieces of 10 k-steps), the other CUs
+  // start on whole tiles and stay a piece's time ahead, so that the rounds'
+  // epilogues no longer store at the same moment on every CU (O projection
+  // 577 -> 563 us; whole tiles first, then the pieces, in two launches before).
   const int full = tiles - tail;
-  if (full > 0) {
-    a.nsplit = 1;
-    KERNEL::launch(full, a, stream);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   a.tile_base = full;
   a.nsplit = nsplit;
-  KERNEL::launch(tail * nsplit, a, stream);
+  a.npieces = tail * nsplit;
+  KERNEL::launch(tail * nsplit + full, a, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t threads = static_cast<int64_t>(tail) * BM * (BN / 4);

@@ -33,9 +33,11 @@ struct GemmBf16Args {
   int res_bf16;
   float* part;              // optional: fp32 partial tiles of the split-K tail
   size_t part_bytes;
-  // set by the launcher: first tile of a launch, k splits per tile (<= 1: the
-  // whole k range), k-steps per split
+  // set by the launcher: the first split tile, k splits per split tile (<= 1:
+  // none), k-steps per split, and the workgroups that run split pieces (the
+  // first npieces of the launch; the rest run whole tiles from tile 0)
   int tile_base, nsplit, kps;
+  int npieces;
 };
 
 struct GemmF32Args {
