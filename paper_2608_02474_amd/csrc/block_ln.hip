@@ -8,9 +8,9 @@
 // fp32 with two passes over the registers, and the modulated result is
 // written in the output storage type.  Every access, the modulation vectors
 // included, is a 16-byte vector load or store.  Rows longer than 512 * MAXC
-// elements take the MAXC == 0 variant, which re-reads the row.  fp32 rows of
-// a width that is a multiple of 512 (the second LayerNorm) are shared by the
-// waves of a workgroup instead (modln_rows_wg).
+// elements take the MAXC == 0 variant, which re-reads the row.  fp32 rows
+// (the second LayerNorm) of width 2048, 4096 or 5120 are shared by the waves
+// of a workgroup instead (modln_rows_wg).
 #include <type_traits>
 
 #include "common.h"
@@ -309,7 +309,7 @@ template <typename Tin, typename Tout, int WAVES>
 static hipError_t launch_modln_wg(const char* name, const Tin* x, int M, int D, const float* shift,
                                   const float* scale, float eps, Tout* out, hipStream_t stream) {
   // about 20 waves per CU (two workgroups at D = 5120: one or three were slower)
-  const int per_cu = WAVES < 10 ? 20 / WAVES : 2;
+  const int per_cu = 20 / WAVES;
   const int cap = per_cu * device_cu_count();
   const dim3 grid(static_cast<unsigned>(M < cap ? M : cap));
   return ECHO_LAUNCH(name, (modln_rows_wg<Tin, Tout, WAVES>), grid, dim3(WAVES * 64), 0, stream, x, M, D,
@@ -320,15 +320,11 @@ template <typename Tin, typename Tout>
 static hipError_t launch_modln_t(const char* name, const Tin* x, int M, int D, const float* shift,
                                  const float* scale, float eps, Tout* out, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  if (std::is_same<Tin, float>::value && D % 512 == 0) {
-    switch (D / 512) {
-      case 4: return launch_modln_wg<Tin, Tout, 4>(name, x, M, D, shift, scale, eps, out, stream);
-      case 8: return launch_modln_wg<Tin, Tout, 8>(name, x, M, D, shift, scale, eps, out, stream);
-      case 10: return launch_modln_wg<Tin, Tout, 10>(name, x, M, D, shift, scale, eps, out, stream);
-      case 12: return launch_modln_wg<Tin, Tout, 12>(name, x, M, D, shift, scale, eps, out, stream);
-      case 16: return launch_modln_wg<Tin, Tout, 16>(name, x, M, D, shift, scale, eps, out, stream);
-      default: break;
-    }
+  if (std::is_same<Tin, float>::value) {
+    // the widths built (and tested): 2048, 4096 and 5120
+    if (D == 512 * 4) return launch_modln_wg<Tin, Tout, 4>(name, x, M, D, shift, scale, eps, out, stream);
+    if (D == 512 * 8) return launch_modln_wg<Tin, Tout, 8>(name, x, M, D, shift, scale, eps, out, stream);
+    if (D == 512 * 10) return launch_modln_wg<Tin, Tout, 10>(name, x, M, D, shift, scale, eps, out, stream);
   }
   const dim3 grid((M + kLnWaves - 1) / kLnWaves);
   const int per_lane = (D / 8 + kWave - 1) / kWave;

@@ -234,6 +234,27 @@ def test_block_partial_full_compare(w):
         check_block(got, want, w.dtype, f"{w.name}/{name}")
 
 
+# widths whose second LayerNorm (over fp32 rows) runs one row per workgroup of
+# D / 512 waves: the widths the kernel is built for other than 5120 (which the
+# full-size tests cover), bf16 and fp32 block
+WIDE = [synth.Workload(f"width{D}_{dt}_60tok", T=1, grid=(6, 10), D=D, H=D // 128, F=512,
+                       n_samples=4000, ratio=0.5, dtype=dt, audio="bursts", seed=90 + D // 512)
+        for D, dt in [(2048, "bf16"), (4096, "bf16"), (2048, "f32")]]
+
+
+@pytest.mark.parametrize("w", WIDE, ids=lambda w: w.name)
+def test_block_partial_ln2_widths(w):
+    p = synth.make_block_weights(w)
+    _, x = synth.make_latents(w)
+    rng = np.random.default_rng(13)
+    kv = OB.kv_projection(OB._f64(p), np.asarray(x, np.float64))
+    for name, idx in {"half": np.sort(rng.choice(w.L, w.L // 2, replace=False)), "one": np.array([w.L - 1])}.items():
+        say(f"block {w.name} {name} n={len(idx)}")
+        got = _block_gpu(w, p, x, idx)
+        want = OB.block_partial(p, x, idx, w.H, kv=kv)
+        check_block(got, want, w.dtype, f"{w.name}/{name}")
+
+
 # bf16 shapes at the edges of the attention tiling: one ragged key tile, exactly
 # one tile, one tile plus one key, three tiles, and query sets that cross a
 # 384-query workgroup (with the key-split tail of a few items)
