@@ -476,14 +476,21 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   const int tiles = ((a.M + BM - 1) / BM) * (a.N / BN);
   const int nk = a.K / BK;
   // Tiles beyond the last full round (one workgroup per CU) are split along
-  // k so that together they fill that round; a reduce kernel adds the splits.
+  // k; a reduce kernel adds the splits.  A tail of at least a quarter of the
+  // CUs is cut so that its pieces fill that round; a smaller one into about
+  // 3/16 of the CUs' worth of pieces (with 256 CUs, measured in the cached
+  // block step: 64 tail tiles in 4 pieces each beat 3, 2 and 1; 16 tiles in
+  // 3 beat 2, 4 and 8 (O projection 562 -> 545 us, FFN down 1377 -> 1331
+  // us); 8 tiles in 6 beat 4 and 8; 4 tiles in the 8 that the k-step floor
+  // below allows beat 6, 4 and 3).
   const int ncu = device_cu_count();
   const int tail = tiles % ncu;
-  int nsplit = tail > 0 ? ncu / tail : 1;
+  int nsplit = 1;
+  if (tail > 0) nsplit = 4 * tail >= ncu ? ncu / tail : (3 * ncu / 16 + tail - 1) / tail;
   nsplit = nsplit < nk ? nsplit : nk;
   // Each split also writes and the reduce reads a 256 KB fp32 partial tile:
-  // below about 20 k-steps per split that costs more than the shorter range
-  // saves (160 k-steps: 8 splits beat 16 by 7-11 us; 432: 16 beat 8).
+  // below about 640 of depth (10 k-steps) per split that costs more than the
+  // shorter range saves.
   constexpr int kMinStepsPerSplit = 640 / BK;
   const int cap = nk / kMinStepsPerSplit > 1 ? nk / kMinStepsPerSplit : 1;
   nsplit = nsplit < cap ? nsplit : cap;
@@ -501,10 +508,11 @@ hipError_t launch_gemm_epi(const char* name, GemmBf16Args a, hipStream_t stream)
   a.kps = (nk + nsplit - 1) / nsplit;  // k-steps per split
   nsplit = (nk + a.kps - 1) / a.kps;   // every split non-empty
   // One launch, the pieces first: when they cover only part of the CUs (the
-  // 13104-row projections: 16 tiles x 8 pieces of 10 k-steps), the other CUs
-  // start on whole tiles and stay a piece's time ahead, so that the rounds'
-  // epilogues no longer store at the same moment on every CU (O projection
-  // 577 -> 563 us; whole tiles first, then the pieces, in two launches before).
+  // 13104-row projections: 16 tiles x 3 pieces), the other CUs start on whole
+  // tiles and stay a piece's time ahead, so that the rounds' epilogues no
+  // longer store at the same moment on every CU (O projection with 8 pieces a
+  // tile: 577 -> 563 us against whole tiles first, then the pieces, in two
+  // launches).
   const int full = tiles - tail;
   a.tile_base = full;
   a.nsplit = nsplit;
