@@ -172,19 +172,6 @@ struct AttList {
   __host__ __device__ int owner(int y, int G) const { return ((y + 1) * G - 1) / w.total; }
 };
 
-// lds_copy16_s on the lanes of exec & exec_mask (exec_mask wave-uniform); the
-// copy counts once in vmcnt whatever the lanes
-__device__ __forceinline__ void lds_copy16_s_exec(const void* sbase, uint32_t voff, uint32_t lds_base,
-                                                  uint64_t exec_mask) {
-  uint64_t saved;
-  asm volatile(
-      "s_mov_b64 %0, exec\n\ts_and_b64 exec, exec, %4\n\ts_mov_b32 m0, %3\n\t"
-      "global_load_lds_dwordx4 %1, %2\n\ts_mov_b64 exec, %0"
-      : "=&s"(saved)
-      : "v"(voff), "s"(sbase), "s"(lds_base), "s"(exec_mask)
-      : "memory", "m0");
-}
-
 #define ECHO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
 #define ECHO_LDS_V4(p) ((__attribute__((address_space(3))) v4i16*)(p))

@@ -214,6 +214,18 @@ __device__ __forceinline__ void lds_copy16_s(const void* sbase, uint32_t voff, u
                : "v"(voff), "s"(sbase), "s"(lds_base)
                : "memory", "m0");
 }
+// lds_copy16_s on the lanes of exec & exec_mask (exec_mask wave-uniform); the
+// copy counts once in vmcnt whatever the lanes
+__device__ __forceinline__ void lds_copy16_s_exec(const void* sbase, uint32_t voff, uint32_t lds_base,
+                                                  uint64_t exec_mask) {
+  uint64_t saved;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\ts_and_b64 exec, exec, %4\n\ts_mov_b32 m0, %3\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\ts_mov_b64 exec, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(sbase), "s"(lds_base), "s"(exec_mask)
+      : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 // s_waitcnt immediate (gfx9 layout) that waits until at most n vector-memory
